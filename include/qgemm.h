@@ -1,0 +1,182 @@
+/*
+ * qgemm.h -- C ABI of the MI355X (gfx950) low-bit quantized-linear library.
+ *
+ * The library implements the quantized linear layers that the paper's
+ * recipe puts on low-precision matrix units (Sec. 4, quantization paragraph;
+ * effect in Table 2): post-training quantization of weights AND runtime
+ * quantization of activations, in two formats the paper cites there:
+ *
+ *   FP8  : E4M3 codes (bias 7, largest finite 448, no infinities), one fp32
+ *          decode scale per tensor:   x ~ e4m3(q) * s.
+ *   NVFP4: E2M1 codes (0, .5, 1, 1.5, 2, 3, 4, 6 and negatives) in blocks of
+ *          16 consecutive elements along a row, one E4M3 scale per block and
+ *          one fp32 decode scale per tensor:  x ~ e2m1(q) * e4m3(s_b) * s_t.
+ *
+ * and a weight-only variant (bf16 activations times NVFP4 weights).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every tensor pointer is a DEVICE pointer on the current HIP device.
+ *    The caller allocates and owns every buffer; the library allocates
+ *    nothing and keeps no state besides its loaded code objects.
+ *  - Matrices are row-major. A "row" runs along the reduction dimension K of
+ *    a linear layer: activations X are [M, K], weights W are [N, K] (the
+ *    nn.Linear layout), outputs Y are [M, N].
+ *  - bf16 data are 16-bit bfloat16 bit patterns; `ld*` arguments count
+ *    elements between consecutive rows (>= the row length).
+ *  - FP8 codes: one byte per element, dense [rows, cols].
+ *  - NVFP4 codes: two per byte, dense [rows, cols/2]; element 2i of a row
+ *    sits in the low nibble of byte i. Block scales: E4M3 bytes, dense
+ *    [rows, cols/16]; block j covers elements 16j .. 16j+15 of its row.
+ *  - Tensor scales are single fp32 values in device memory (decode scales).
+ *  - All work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *    stream) with no host synchronisation. Argument and shape checks run on
+ *    the host before anything is enqueued and report through the return
+ *    value; a failed check enqueues nothing. Errors of the HIP runtime are
+ *    reported as QG_ERR_HIP (see qg_last_hip_error). Calls are thread-safe;
+ *    calls whose buffers overlap must be ordered by the caller's streams.
+ *  - Non-finite inputs are outside the contract: a tensor holding inf/NaN
+ *    gets a NaN tensor scale (a sentinel a caller can test) and
+ *    unspecified codes.
+ */
+#ifndef QGEMM_H
+#define QGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QG_ABI_VERSION 1
+
+typedef enum qg_status {
+    QG_OK = 0,
+    QG_ERR_INVALID_ARG = 1,      /* null pointer, bad enum, negative size, ld too small */
+    QG_ERR_UNSUPPORTED = 2,      /* format or format pair the library does not implement */
+    QG_ERR_SHAPE = 3,            /* shape breaks the layout contract (e.g. K % 16 for NVFP4) */
+    QG_ERR_BUFFER_TOO_SMALL = 4, /* a size argument is smaller than the data it must hold */
+    QG_ERR_HIP = 5               /* the HIP runtime reported an error */
+} qg_status;
+
+typedef enum qg_format {
+    QG_FMT_BF16 = 0,             /* unquantized bfloat16 */
+    QG_FMT_FP8_E4M3 = 1,         /* E4M3 codes + per-tensor fp32 scale */
+    QG_FMT_NVFP4 = 2             /* E2M1 codes + E4M3 per-16 block scales + fp32 tensor scale */
+} qg_format;
+
+typedef enum qg_out_dtype {
+    QG_OUT_BF16 = 0,             /* round-to-nearest-even bfloat16 */
+    QG_OUT_F32 = 1               /* IEEE binary32 */
+} qg_out_dtype;
+
+/*
+ * qg_quantize_act -- dynamic quantization of a bf16 tensor (activations at
+ * run time, weights offline before qg_pack_weights: the same arithmetic).
+ * Paper: Sec. 4, quantization paragraph (activation quantization is what
+ * lets the linears run on low-precision units; PTQ of weights).
+ *
+ *   fmt           QG_FMT_FP8_E4M3 or QG_FMT_NVFP4.
+ *   x             bf16 [rows, ldx], the first `cols` of each row are used.
+ *   codes         out: FP8 [rows, cols] bytes; NVFP4 [rows, cols/2] bytes.
+ *   block_scales  out: NVFP4 [rows, cols/16] E4M3 bytes; must be NULL for FP8.
+ *   tensor_scale  out: one fp32 decode scale. It doubles as the scratch slot
+ *                 of the tensor-wide max reduction, so it must not alias
+ *                 the other buffers.
+ *
+ * Arithmetic (bit-exact; every step one IEEE binary32 operation, RNE):
+ *   FP8  : a = max|x|; s = a/448; r = s>0 ? 1/s : 0; q = E4M3(x*r)
+ *   NVFP4: a = max|x|; s_t = a/2688; d = 6*s_t; per block b:
+ *          v = d>0 ? max_b|x|/d : 0; s_b = E4M3(v); S = e4m3(s_b)*s_t;
+ *          r = S>0 ? 1/S : 0; q = E2M1(x*r)
+ *   E4M3()/E2M1() round to nearest, ties to the even code, saturate at
+ *   +-448 / +-6, and keep the sign of zero.
+ * Shapes: rows, cols >= 0; NVFP4 needs cols % 16 == 0 (QG_ERR_SHAPE).
+ * An empty tensor gets tensor_scale = 0.
+ */
+qg_status qg_quantize_act(qg_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                          void *codes, void *block_scales, float *tensor_scale, void *stream);
+
+/*
+ * qg_packed_bytes -- size of the packed weight buffer for an [n, k] weight
+ * in `fmt` (FP8 or NVFP4), or 0 when the shape breaks the GEMM contract
+ * (n % 16, k % 128) or the format is not packable.
+ */
+size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
+
+/*
+ * qg_pack_weights -- offline re-layout of a quantized weight W [n, k] into
+ * the order in which the GEMM's matrix-core operands consume it, plus a
+ * small header holding the format, n, k and a copy of the tensor scale.
+ * Paper: Sec. 4, quantization paragraph (PTQ weights are prepared once,
+ * like the cached engines of Sec. 5).
+ *
+ *   codes, block_scales, tensor_scale: as written by qg_quantize_act
+ *                 (block_scales NULL for FP8).
+ *   packed        out: qg_packed_bytes(fmt, n, k) bytes, 256-byte aligned.
+ * The layout is private to this library version (qg_unpack_weights is its
+ * exact inverse). Shapes: n % 16 == 0 and k % 128 == 0, else QG_ERR_SHAPE.
+ */
+qg_status qg_pack_weights(qg_format fmt, const void *codes, const void *block_scales,
+                          const float *tensor_scale, int64_t n, int64_t k,
+                          void *packed, size_t packed_bytes, void *stream);
+
+/*
+ * qg_unpack_weights -- inverse of qg_pack_weights: writes the canonical
+ * codes, block scales (NVFP4) and tensor scale back out. For tests and for
+ * tools that need the weights in the canonical layout.
+ */
+qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_bytes,
+                            int64_t n, int64_t k, void *codes, void *block_scales,
+                            float *tensor_scale, void *stream);
+
+/*
+ * qg_gemm -- quantized linear layer Y = deq(A) . deq(W)^T.
+ * Paper: Sec. 4, quantization paragraph; Table 2 (FP8 and NVFP4 linears of
+ * the denoising transformer); weight-only NVFP4 for the small encoder path.
+ *
+ * Supported (a_fmt, w_fmt) pairs, else QG_ERR_UNSUPPORTED:
+ *   (FP8_E4M3, FP8_E4M3)  W8A8:  a = codes [m, k] (lda = k), a_block_scales NULL
+ *   (NVFP4,    NVFP4)     W4A4:  a = codes [m, k/2], a_block_scales [m, k/16] (lda = k)
+ *   (BF16,     NVFP4)     W4A16: a = bf16 [m, lda], a_block_scales and a_tensor_scale NULL
+ *   a_tensor_scale  device fp32 decode scale of A (quantized formats).
+ *   w_packed        buffer written by qg_pack_weights for an [n, k] weight.
+ *   y               out: [m, ldy] of y_dtype.
+ * Result: y[i,j] = s_a * s_w * sum_k deq'(a)[i,k] deq'(w)[j,k] with fp32
+ * accumulation (deq' = decoded codes times block scales; the tensor scales
+ * are applied once at the end), then rounded to y_dtype. Accuracy contract:
+ * |y - y_exact| <= 1e-3 * sum_k |a w| plus the rounding of y to y_dtype.
+ * Shapes: m, n, k >= 0; n % 16 == 0; k % 128 == 0; lda >= k, ldy >= n.
+ */
+qg_status qg_gemm(qg_format a_fmt, const void *a, const void *a_block_scales,
+                  const float *a_tensor_scale, int64_t lda,
+                  qg_format w_fmt, const void *w_packed, size_t w_packed_bytes,
+                  int64_t m, int64_t n, int64_t k,
+                  void *y, int64_t ldy, qg_out_dtype y_dtype, void *stream);
+
+/*
+ * qg_dequant -- decode a quantized tensor to bf16 or fp32.
+ *   FP8  : out = fl(e4m3(q) * s)
+ *   NVFP4: out = fl(fl(e2m1(q) * e4m3(s_b)) * s_t)   (the inner product is exact)
+ * bf16 output is the RNE rounding of that fp32 value. out is dense
+ * [rows, cols]. NVFP4 needs cols % 16 == 0.
+ */
+qg_status qg_dequant(qg_format fmt, const void *codes, const void *block_scales,
+                     const float *tensor_scale, int64_t rows, int64_t cols,
+                     void *out, qg_out_dtype out_dtype, void *stream);
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char *qg_status_string(qg_status s);
+
+/* The HIP error code behind the most recent QG_ERR_HIP on this thread (0 if none). */
+int qg_last_hip_error(void);
+
+/* QG_ABI_VERSION of the built library. */
+int qg_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QGEMM_H */

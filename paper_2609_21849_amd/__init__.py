@@ -1,0 +1,220 @@
+"""MI355X (gfx950) low-bit quantized linear layers: Python binding of libqgemm.so.
+
+The functions named ``qg_*`` mirror the C ABI in ``include/qgemm.h`` one to
+one and only marshal arguments: torch tensors become device pointers, None
+becomes NULL, and the stream defaults to torch's current stream. Every step
+of the computation runs in the HIP kernels of ``libqgemm.so``; if the library
+is missing this module raises instead of computing anything elsewhere.
+
+A few helpers below (``quantize``, ``pack``, ``linear`` ...) allocate the
+output tensors with torch and then call the same entry points.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libqgemm.so")
+
+QG_FMT_BF16, QG_FMT_FP8_E4M3, QG_FMT_NVFP4 = 0, 1, 2
+QG_OUT_BF16, QG_OUT_F32 = 0, 1
+QG_OK = 0
+STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
+                4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
+EXPORTS = ["qg_quantize_act", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
+           "qg_dequant", "qg_status_string", "qg_last_hip_error", "qg_abi_version"]
+
+
+class QGError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s" % (where, STATUS_NAMES.get(status, status)))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libqgemm.so; raise loudly when it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libqgemm.so is not built (run `python -m paper_2609_21849_amd.build` "
+                              "or __graft_entry__.build()); there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+        L.qg_quantize_act.restype = I32
+        L.qg_quantize_act.argtypes = [I32, P, I64, I64, I64, P, P, P, P]
+        L.qg_packed_bytes.restype = SZ
+        L.qg_packed_bytes.argtypes = [I32, I64, I64]
+        L.qg_pack_weights.restype = I32
+        L.qg_pack_weights.argtypes = [I32, P, P, P, I64, I64, P, SZ, P]
+        L.qg_unpack_weights.restype = I32
+        L.qg_unpack_weights.argtypes = [I32, P, SZ, I64, I64, P, P, P, P]
+        L.qg_gemm.restype = I32
+        L.qg_gemm.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, I32, P]
+        L.qg_dequant.restype = I32
+        L.qg_dequant.argtypes = [I32, P, P, P, I64, I64, P, I32, P]
+        L.qg_status_string.restype = ctypes.c_char_p
+        L.qg_status_string.argtypes = [I32]
+        L.qg_last_hip_error.restype = I32
+        L.qg_abi_version.restype = I32
+        _lib = L
+    return _lib
+
+
+def _p(t) -> int | None:
+    """Device pointer of a tensor (or an int pointer); None -> NULL."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int, where: str) -> None:
+    if status != QG_OK:
+        raise QGError(status, where)
+
+
+# ---------------------------------------------------------------- the C ABI, one to one
+def qg_quantize_act(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale, stream=None, check=True):
+    s = lib().qg_quantize_act(fmt, _p(x), rows, cols, ldx, _p(codes), _p(block_scales), _p(tensor_scale), _stream(stream))
+    if check:
+        _check(s, "qg_quantize_act")
+    return s
+
+
+def qg_packed_bytes(fmt, n, k) -> int:
+    return lib().qg_packed_bytes(fmt, n, k)
+
+
+def qg_pack_weights(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes, stream=None, check=True):
+    s = lib().qg_pack_weights(fmt, _p(codes), _p(block_scales), _p(tensor_scale), n, k, _p(packed), packed_bytes, _stream(stream))
+    if check:
+        _check(s, "qg_pack_weights")
+    return s
+
+
+def qg_unpack_weights(fmt, packed, packed_bytes, n, k, codes, block_scales, tensor_scale, stream=None, check=True):
+    s = lib().qg_unpack_weights(fmt, _p(packed), packed_bytes, n, k, _p(codes), _p(block_scales), _p(tensor_scale), _stream(stream))
+    if check:
+        _check(s, "qg_unpack_weights")
+    return s
+
+
+def qg_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_packed_bytes, m, n, k,
+            y, ldy, y_dtype, stream=None, check=True):
+    s = lib().qg_gemm(a_fmt, _p(a), _p(a_block_scales), _p(a_tensor_scale), lda, w_fmt, _p(w_packed),
+                      w_packed_bytes, m, n, k, _p(y), ldy, y_dtype, _stream(stream))
+    if check:
+        _check(s, "qg_gemm")
+    return s
+
+
+def qg_dequant(fmt, codes, block_scales, tensor_scale, rows, cols, out, out_dtype, stream=None, check=True):
+    s = lib().qg_dequant(fmt, _p(codes), _p(block_scales), _p(tensor_scale), rows, cols, _p(out), out_dtype, _stream(stream))
+    if check:
+        _check(s, "qg_dequant")
+    return s
+
+
+def qg_status_string(status: int) -> str:
+    return lib().qg_status_string(status).decode()
+
+
+def qg_last_hip_error() -> int:
+    return lib().qg_last_hip_error()
+
+
+def qg_abi_version() -> int:
+    return lib().qg_abi_version()
+
+
+# ---------------------------------------------------------------- allocating helpers
+@dataclass
+class QTensor:
+    """A quantized tensor on the GPU: codes, block scales (NVFP4) and the fp32 tensor scale."""
+    fmt: int
+    codes: "object"
+    block_scales: "object"
+    tensor_scale: "object"
+    rows: int
+    cols: int
+
+
+def quantize(x, fmt: int, stream=None) -> QTensor:
+    """Quantize a [rows, cols] bf16 CUDA tensor (row stride may exceed cols)."""
+    import torch
+    assert x.dtype == torch.bfloat16 and x.dim() == 2 and x.stride(1) == 1
+    rows, cols = x.shape
+    dev = x.device
+    if fmt == QG_FMT_FP8_E4M3:
+        codes = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+        bs = None
+    else:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
+        bs = torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev)
+    ts = torch.empty(1, dtype=torch.float32, device=dev)
+    qg_quantize_act(fmt, x, rows, cols, x.stride(0), codes, bs, ts, stream)
+    return QTensor(fmt, codes, bs, ts, rows, cols)
+
+
+def pack(q: QTensor, stream=None):
+    """Pack a quantized weight [n, k] for qg_gemm; returns a uint8 CUDA tensor."""
+    import torch
+    nbytes = qg_packed_bytes(q.fmt, q.rows, q.cols)
+    if nbytes == 0:
+        raise QGError(3, "qg_packed_bytes")
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=q.codes.device)
+    qg_pack_weights(q.fmt, q.codes, q.block_scales, q.tensor_scale, q.rows, q.cols, packed, nbytes, stream)
+    return packed
+
+
+def unpack(packed, fmt: int, n: int, k: int, stream=None) -> QTensor:
+    import torch
+    dev = packed.device
+    if fmt == QG_FMT_FP8_E4M3:
+        codes, bs = torch.empty((n, k), dtype=torch.uint8, device=dev), None
+    else:
+        codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev)
+        bs = torch.empty((n, k // 16), dtype=torch.uint8, device=dev)
+    ts = torch.empty(1, dtype=torch.float32, device=dev)
+    qg_unpack_weights(fmt, packed, packed.numel(), n, k, codes, bs, ts, stream)
+    return QTensor(fmt, codes, bs, ts, n, k)
+
+
+def linear(a, w_packed, w_fmt: int, n: int, out_dtype: int = QG_OUT_BF16, y=None, stream=None):
+    """Y = A . W^T for a quantized A (QTensor) or a bf16 A (torch tensor)."""
+    import torch
+    if isinstance(a, QTensor):
+        m, k, a_fmt = a.rows, a.cols, a.fmt
+        a_data, a_bs, a_ts, lda = a.codes, a.block_scales, a.tensor_scale, a.cols
+        dev = a.codes.device
+    else:
+        m, k = a.shape
+        a_fmt, a_data, a_bs, a_ts, lda = QG_FMT_BF16, a, None, None, a.stride(0)
+        dev = a.device
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16, device=dev)
+    qg_gemm(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, y, y.stride(0), out_dtype, stream)
+    return y
+
+
+def dequantize(q: QTensor, out_dtype: int = QG_OUT_F32, stream=None):
+    import torch
+    out = torch.empty((q.rows, q.cols), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16,
+                      device=q.codes.device)
+    qg_dequant(q.fmt, q.codes, q.block_scales, q.tensor_scale, q.rows, q.cols, out, out_dtype, stream)
+    return out

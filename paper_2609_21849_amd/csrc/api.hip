@@ -1,0 +1,172 @@
+// api.hip -- the C ABI declared in include/qgemm.h.
+//
+// Every entry point validates its arguments on the host, then only enqueues
+// kernels on the caller's stream. Nothing here allocates device memory or
+// synchronises. A failed check returns before any HIP call, which is why
+// these checks can be exercised on a machine without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <limits>
+
+#include "kernels.hpp"
+#include "qgemm.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+qg_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return QG_OK;
+  g_last_hip_error = (int)e;
+  return QG_ERR_HIP;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool valid_fmt(int f) { return f == QG_FMT_BF16 || f == QG_FMT_FP8_E4M3 || f == QG_FMT_NVFP4; }
+
+constexpr int64_t kMaxDim = std::numeric_limits<int32_t>::max();
+
+}  // namespace
+
+extern "C" {
+
+const char* qg_status_string(qg_status s) {
+  switch (s) {
+    case QG_OK: return "ok";
+    case QG_ERR_INVALID_ARG: return "invalid argument";
+    case QG_ERR_UNSUPPORTED: return "unsupported format";
+    case QG_ERR_SHAPE: return "shape breaks the layout contract";
+    case QG_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case QG_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int qg_last_hip_error(void) { return g_last_hip_error; }
+
+int qg_abi_version(void) { return QG_ABI_VERSION; }
+
+qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
+                          void* codes, void* block_scales, float* tensor_scale, void* stream) {
+  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
+  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+  const bool empty = (rows == 0 || cols == 0);
+  if (!empty) {
+    if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+  }
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols,
+                                        ldx, reinterpret_cast<uint8_t*>(codes),
+                                        reinterpret_cast<uint8_t*>(block_scales), tensor_scale, st));
+}
+
+size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k) {
+  if (fmt != QG_FMT_FP8_E4M3 && fmt != QG_FMT_NVFP4) return 0;
+  if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim || n % 16 != 0 || k % 128 != 0) return 0;
+  return (size_t)qg::packed_total_bytes((int)fmt, n, k);
+}
+
+static qg_status check_pack_args(qg_format fmt, const void* codes, const void* block_scales,
+                                 const void* tensor_scale, int64_t n, int64_t k,
+                                 const void* packed, size_t packed_bytes) {
+  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
+  if (packed == nullptr || tensor_scale == nullptr || !aligned(packed, 256) || !aligned(tensor_scale, 4))
+    return QG_ERR_INVALID_ARG;
+  if (packed_bytes < (size_t)qg::packed_total_bytes((int)fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
+  if (n > 0 && k > 0) {
+    if (codes == nullptr || !aligned(codes, 16)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(block_scales, 8))) return QG_ERR_INVALID_ARG;
+  }
+  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+  return QG_OK;
+}
+
+qg_status qg_pack_weights(qg_format fmt, const void* codes, const void* block_scales,
+                          const float* tensor_scale, int64_t n, int64_t k, void* packed,
+                          size_t packed_bytes, void* stream) {
+  const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
+  if (s != QG_OK) return s;
+  return hip_status(qg::launch_pack((int)fmt, reinterpret_cast<const uint8_t*>(codes),
+                                    reinterpret_cast<const uint8_t*>(block_scales), tensor_scale, n,
+                                    k, reinterpret_cast<uint8_t*>(packed),
+                                    reinterpret_cast<hipStream_t>(stream)));
+}
+
+qg_status qg_unpack_weights(qg_format fmt, const void* packed, size_t packed_bytes, int64_t n,
+                            int64_t k, void* codes, void* block_scales, float* tensor_scale,
+                            void* stream) {
+  const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
+  if (s != QG_OK) return s;
+  return hip_status(qg::launch_unpack((int)fmt, reinterpret_cast<const uint8_t*>(packed), n, k,
+                                      reinterpret_cast<uint8_t*>(codes),
+                                      reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                      reinterpret_cast<hipStream_t>(stream)));
+}
+
+qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
+                  const float* a_tensor_scale, int64_t lda, qg_format w_fmt, const void* w_packed,
+                  size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y, int64_t ldy,
+                  qg_out_dtype y_dtype, void* stream) {
+  if (!valid_fmt(a_fmt) || !valid_fmt(w_fmt)) return QG_ERR_INVALID_ARG;
+  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+  const bool w8a8 = (a_fmt == QG_FMT_FP8_E4M3 && w_fmt == QG_FMT_FP8_E4M3);
+  const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
+  const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
+  if (!(w8a8 || w4a4 || w4a16)) return QG_ERR_UNSUPPORTED;
+  if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
+  if (m > 0 && lda < k) return QG_ERR_INVALID_ARG;
+  if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
+  if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
+  if (w_packed_bytes < (size_t)qg::packed_total_bytes((int)w_fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
+  if (m > 0 && n > 0) {
+    if (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2)) return QG_ERR_INVALID_ARG;
+    if (k > 0) {
+      if (a == nullptr) return QG_ERR_INVALID_ARG;
+      if (w8a8 && (!aligned(a, 16) || lda % 16 != 0 || a_tensor_scale == nullptr || a_block_scales != nullptr))
+        return QG_ERR_INVALID_ARG;
+      if (w4a4 && (!aligned(a, 16) || lda != k || a_tensor_scale == nullptr || a_block_scales == nullptr ||
+                   !aligned(a_block_scales, 8)))
+        return QG_ERR_INVALID_ARG;
+      if (w4a16 && (!aligned(a, 16) || lda % 8 != 0 || a_tensor_scale != nullptr || a_block_scales != nullptr))
+        return QG_ERR_INVALID_ARG;
+    }
+  }
+  return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
+                                    a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
+                                    n, k, y, ldy, y_dtype == QG_OUT_F32,
+                                    reinterpret_cast<hipStream_t>(stream)));
+}
+
+qg_status qg_dequant(qg_format fmt, const void* codes, const void* block_scales,
+                     const float* tensor_scale, int64_t rows, int64_t cols, void* out,
+                     qg_out_dtype out_dtype, void* stream) {
+  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (out_dtype != QG_OUT_BF16 && out_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+  if (rows > 0 && cols > 0) {
+    if (codes == nullptr || out == nullptr || !aligned(out, out_dtype == QG_OUT_F32 ? 4 : 2))
+      return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+  }
+  return hip_status(qg::launch_dequant((int)fmt, reinterpret_cast<const uint8_t*>(codes),
+                                       reinterpret_cast<const uint8_t*>(block_scales), tensor_scale,
+                                       rows, cols, out, out_dtype == QG_OUT_F32,
+                                       reinterpret_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

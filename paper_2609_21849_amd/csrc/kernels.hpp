@@ -1,0 +1,41 @@
+// kernels.hpp -- internal launchers shared by the C-ABI layer (api.hip).
+// Each launcher only enqueues work on `st`; arguments were validated by the
+// caller. Format ids follow qg_format: 0 bf16, 1 FP8 E4M3, 2 NVFP4.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace qg {
+
+// Packed weight buffer: a 256-byte header, then the codes region, then (for
+// NVFP4) the block-scale region. Header fields (little endian):
+//   +0 u32 magic 'QGPW', +4 u32 layout version, +8 u32 format,
+//   +16 i64 n, +24 i64 k, +32 f32 tensor decode scale.
+constexpr uint32_t kPackMagic = 0x57504751u;  // "QGPW"
+constexpr uint32_t kPackVersion = 1u;
+constexpr int64_t kPackHeader = 256;
+constexpr int64_t kPackScaleOffset = 32;
+
+inline int64_t packed_codes_bytes(int fmt, int64_t n, int64_t k) {
+  return fmt == 1 ? n * k : n * k / 2;
+}
+inline int64_t packed_total_bytes(int fmt, int64_t n, int64_t k) {
+  return kPackHeader + packed_codes_bytes(fmt, n, k) + (fmt == 2 ? n * k / 16 : 0);
+}
+
+hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                           uint8_t* codes, uint8_t* bscale, float* tscale, hipStream_t st);
+hipError_t launch_dequant(int fmt, const uint8_t* codes, const uint8_t* bscale, const float* tscale,
+                          int64_t rows, int64_t cols, void* out, bool f32out, hipStream_t st);
+hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, const float* tscale,
+                       int64_t n, int64_t k, uint8_t* packed, hipStream_t st);
+hipError_t launch_unpack(int fmt, const uint8_t* packed, int64_t n, int64_t k, uint8_t* codes,
+                         uint8_t* bscale, float* tscale, hipStream_t st);
+hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const float* a_tscale,
+                       int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
+                       void* y, int64_t ldy, bool f32out, hipStream_t st);
+
+}  // namespace qg

@@ -1,0 +1,138 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/qgemm.h declares, and rejects bad arguments on the host with the
+documented status codes before any HIP call.
+
+Every call below is built to FAIL validation (fake pointers are never
+dereferenced), so the tests are also safe on a machine with a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_21849_amd as q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qgemm.h")
+
+OK, INVALID, UNSUP, SHAPE, SMALL = 0, 1, 2, 3, 4
+FP8, NVFP4, BF16 = q.QG_FMT_FP8_E4M3, q.QG_FMT_NVFP4, q.QG_FMT_BF16
+P = 0x10000  # a fake, 64 KiB-aligned "device pointer" that validation never dereferences
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qg_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 9
+    L = ctypes.CDLL(q.LIB_PATH)
+    for name in names:
+        assert hasattr(L, name), name
+    assert sorted(names) == sorted(q.EXPORTS)
+
+
+def test_abi_version_and_status_strings():
+    assert q.qg_abi_version() == 1
+    for s in range(6):
+        assert q.qg_status_string(s)
+    assert q.qg_status_string(OK) == "ok"
+    assert q.qg_last_hip_error() == 0
+
+
+def test_packed_bytes():
+    assert q.qg_packed_bytes(FP8, 256, 256) == 256 + 256 * 256
+    assert q.qg_packed_bytes(NVFP4, 3072, 3072) == 256 + 3072 * 3072 // 2 + 3072 * 3072 // 16
+    assert q.qg_packed_bytes(NVFP4, 0, 0) == 256
+    assert q.qg_packed_bytes(FP8, 24, 256) == 0      # n % 16
+    assert q.qg_packed_bytes(FP8, 256, 192) == 0     # k % 128
+    assert q.qg_packed_bytes(BF16, 256, 256) == 0
+    assert q.qg_packed_bytes(7, 256, 256) == 0
+
+
+def _quant(fmt, x=P, rows=4, cols=32, ldx=32, codes=P, bs=P, ts=P):
+    return q.qg_quantize_act(fmt, x, rows, cols, ldx, codes, bs, ts, stream=0, check=False)
+
+
+def test_quantize_validation():
+    assert _quant(9) == INVALID
+    assert _quant(BF16) == UNSUP
+    assert _quant(NVFP4, cols=24, ldx=24) == SHAPE
+    assert _quant(NVFP4, ts=None) == INVALID
+    assert _quant(NVFP4, x=None) == INVALID
+    assert _quant(NVFP4, bs=None) == INVALID
+    assert _quant(NVFP4, codes=P + 4) == INVALID          # codes need 8-byte alignment
+    assert _quant(NVFP4, ldx=16) == INVALID               # ldx < cols
+    assert _quant(NVFP4, rows=-1) == INVALID
+    assert _quant(FP8, bs=P) == INVALID                   # FP8 has no block scales
+    assert _quant(FP8, bs=None, x=P + 1) == INVALID       # bf16 needs 2-byte alignment
+    assert _quant(FP8, bs=None, ts=P + 2) == INVALID
+
+
+def _pack(fmt, codes=P, bs=P, ts=P, n=32, k=128, packed=P, nbytes=1 << 20, unpack=False):
+    if unpack:
+        return q.qg_unpack_weights(fmt, packed, nbytes, n, k, codes, bs, ts, stream=0, check=False)
+    return q.qg_pack_weights(fmt, codes, bs, ts, n, k, packed, nbytes, stream=0, check=False)
+
+
+@pytest.mark.parametrize("unpack", [False, True])
+def test_pack_validation(unpack):
+    assert _pack(5, unpack=unpack) == INVALID
+    assert _pack(BF16, unpack=unpack) == UNSUP
+    assert _pack(NVFP4, n=24, unpack=unpack) == SHAPE
+    assert _pack(NVFP4, k=64, unpack=unpack) == SHAPE
+    assert _pack(NVFP4, nbytes=100, unpack=unpack) == SMALL
+    assert _pack(NVFP4, packed=P + 128, unpack=unpack) == INVALID     # 256-byte alignment
+    assert _pack(NVFP4, codes=P + 8, unpack=unpack) == INVALID
+    assert _pack(NVFP4, bs=None, unpack=unpack) == INVALID
+    assert _pack(FP8, unpack=unpack) == INVALID                       # FP8 with block scales
+    assert _pack(NVFP4, ts=None, unpack=unpack) == INVALID
+
+
+def _gemm(a_fmt=NVFP4, w_fmt=NVFP4, a=P, abs_=P, ats=P, lda=256, wp=P, wbytes=1 << 24,
+          m=32, n=64, k=256, y=P, ldy=64, yd=0):
+    return q.qg_gemm(a_fmt, a, abs_, ats, lda, w_fmt, wp, wbytes, m, n, k, y, ldy, yd, stream=0, check=False)
+
+
+def test_gemm_validation():
+    assert _gemm(a_fmt=7) == INVALID
+    assert _gemm(yd=3) == INVALID
+    assert _gemm(a_fmt=FP8, w_fmt=NVFP4) == UNSUP
+    assert _gemm(a_fmt=NVFP4, w_fmt=FP8) == UNSUP
+    assert _gemm(a_fmt=BF16, w_fmt=BF16) == UNSUP
+    assert _gemm(a_fmt=BF16, w_fmt=FP8) == UNSUP
+    assert _gemm(n=40) == SHAPE
+    assert _gemm(k=200, lda=200) == SHAPE
+    assert _gemm(m=-1) == INVALID
+    assert _gemm(ldy=32) == INVALID
+    assert _gemm(lda=128) == INVALID
+    assert _gemm(wbytes=1000) == SMALL
+    assert _gemm(wp=P + 16) == INVALID
+    assert _gemm(wp=None) == INVALID
+    assert _gemm(y=None) == INVALID
+    assert _gemm(a=None) == INVALID
+    assert _gemm(abs_=None) == INVALID                                   # W4A4 needs A block scales
+    assert _gemm(lda=512) == INVALID                                     # W4A4 codes are dense
+    assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, a=P + 8) == INVALID     # 16-byte alignment
+    assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, ats=None) == INVALID
+    assert _gemm(a_fmt=FP8, w_fmt=FP8) == INVALID                         # FP8 A has no block scales
+    assert _gemm(a_fmt=BF16, abs_=None, ats=P) == INVALID                 # bf16 A has no scales
+    assert _gemm(a_fmt=BF16, abs_=None, ats=None, lda=260) == INVALID      # lda % 8
+
+
+def test_dequant_validation():
+    def dq(fmt, codes=P, bs=P, ts=P, rows=4, cols=32, out=P, od=0):
+        return q.qg_dequant(fmt, codes, bs, ts, rows, cols, out, od, stream=0, check=False)
+    assert dq(8) == INVALID
+    assert dq(BF16) == UNSUP
+    assert dq(NVFP4, cols=20) == SHAPE
+    assert dq(NVFP4, od=5) == INVALID
+    assert dq(NVFP4, ts=None) == INVALID
+    assert dq(NVFP4, bs=None) == INVALID
+    assert dq(NVFP4, out=None) == INVALID
+    assert dq(FP8) == INVALID                                            # FP8 with block scales
+    assert dq(NVFP4, out=P + 2, od=1) == INVALID                          # fp32 out alignment

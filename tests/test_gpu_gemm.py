@@ -1,0 +1,169 @@
+"""GPU parity of qg_gemm with the CPU oracle: every output (or, at the full
+transformer sizes, a large sample of outputs including the tile edges)
+within |y - y_ref| <= 1e-3 * sum_k |a w| of the oracle's fp64 product over
+the same quantized operands. Codes of both operands are checked bit-exact
+on the way."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_21849_amd as q
+import synth
+from gpu_util import DEV, assert_quant_equal, check_linear, host, log, to_dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+FP8, NVFP4, BF16 = q.QG_FMT_FP8_E4M3, q.QG_FMT_NVFP4, q.QG_FMT_BF16
+KINDS = {"fp8": (FP8, FP8), "nvfp4": (NVFP4, NVFP4), "w4a16": (BF16, NVFP4)}
+
+
+def run_linear(kind, x, w, out=q.QG_OUT_BF16, check_codes=True):
+    a_fmt, w_fmt = KINDS[kind]
+    xd, wd = to_dev_bf16(x), to_dev_bf16(w)
+    wq = q.quantize(wd, w_fmt)
+    packed = q.pack(wq)
+    a = xd if a_fmt == BF16 else q.quantize(xd, a_fmt)
+    y = q.linear(a, packed, w_fmt, w.shape[0], out_dtype=out)
+    torch.cuda.synchronize()
+    if check_codes:
+        assert_quant_equal(wq, w)
+        if a_fmt != BF16:
+            assert_quant_equal(a, x)
+    return y
+
+
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4", "w4a16"])
+@pytest.mark.parametrize("m,n,k", [(1, 16, 128), (17, 48, 256), (64, 256, 256), (65, 128, 128),
+                                   (300, 272, 384), (257, 512, 1024), (512, 768, 640)])
+@pytest.mark.parametrize("out", [q.QG_OUT_F32, q.QG_OUT_BF16])
+def test_small_full_parity(kind, m, n, k, out):
+    log("gemm kind=%s m=%d n=%d k=%d out=%d" % (kind, m, n, k, out))
+    x = synth.normal_bf16(m, k, 1.0, 11, 0)
+    w = synth.normal_bf16(n, k, 0.02, 11, 1)
+    y = run_linear(kind, x, w, out)
+    ref = oracle.linear_reference(kind, x, w)
+    check_linear(y, ref)
+
+
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4", "w4a16"])
+def test_structured_one_hot(kind):
+    """X = rows of +-1 at one position per 16-block, W = small integers: every
+    dequantized product is exact and the fp32 output must be exact too
+    (catches any transposition of the matrix-core operand or output layout)."""
+    m, n, k = 48, 64, 256
+    rng = np.random.default_rng(12)
+    xf = np.zeros((m, k), np.float32)
+    for i in range(m):
+        for b in range(k // 16):
+            xf[i, 16 * b + rng.integers(16)] = rng.choice([-1.0, 1.0]) * 4.0
+    wf = rng.integers(-6, 7, size=(n, k)).astype(np.float32)
+    wf[:, 0] = 6.0  # amax 6 in every weight row/block keeps scales powers of two
+    for b in range(k // 16):
+        wf[:, 16 * b] = 6.0
+    x = synth.f32_to_bf16_bits(xf)
+    w = synth.f32_to_bf16_bits(wf)
+    y = run_linear(kind, x, w, q.QG_OUT_F32)
+    ref = oracle.linear_reference(kind, x, w)
+    got = host(y).astype(np.float64)
+    assert np.array_equal(got, ref["y"]), np.argwhere(got != ref["y"])[:5]
+
+
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4", "w4a16"])
+def test_row_of_output_independent_of_batch(kind):
+    """Row m of a 16-row product equals the 1-row product of that row."""
+    x = synth.normal_bf16(16, 1024, 1.0, 13, 0)
+    w = synth.normal_bf16(3072, 1024, 0.02, 13, 1)
+    a_fmt, w_fmt = KINDS[kind]
+    wq = q.quantize(to_dev_bf16(w), w_fmt)
+    packed = q.pack(wq)
+    xd = to_dev_bf16(x)
+    if a_fmt == BF16:
+        y16 = q.linear(xd, packed, w_fmt, 3072, out_dtype=q.QG_OUT_F32)
+        y1 = q.linear(xd[5:6], packed, w_fmt, 3072, out_dtype=q.QG_OUT_F32)
+        torch.cuda.synchronize()
+        assert torch.allclose(y16[5], y1[0], rtol=1e-5, atol=1e-6)
+    else:
+        a = q.quantize(xd, a_fmt)
+        y16 = q.linear(a, packed, w_fmt, 3072, out_dtype=q.QG_OUT_F32)
+        torch.cuda.synchronize()
+        ref = oracle.linear_reference(kind, x, w)
+        check_linear(y16, ref)
+
+
+def test_deterministic():
+    x = synth.normal_bf16(300, 1024, 1.0, 14, 0)
+    w = synth.normal_bf16(512, 1024, 0.02, 14, 1)
+    for kind in ("fp8", "nvfp4", "w4a16"):
+        y1 = run_linear(kind, x, w, check_codes=False)
+        y2 = run_linear(kind, x, w, check_codes=False)
+        assert torch.equal(y1, y2), kind
+
+
+def test_zero_k_and_empty_m():
+    w = torch.zeros((16, 0), dtype=torch.bfloat16, device=DEV)
+    for fmt in (FP8, NVFP4):
+        nbytes = q.qg_packed_bytes(fmt, 16, 0)
+        packed = torch.zeros(nbytes, dtype=torch.uint8, device=DEV)
+        ts = torch.ones(1, dtype=torch.float32, device=DEV)
+        y = torch.full((3, 16), 7.0, dtype=torch.float32, device=DEV)
+        a = torch.zeros(16, dtype=torch.uint8, device=DEV)
+        bs = torch.zeros(16, dtype=torch.uint8, device=DEV)
+        q.qg_gemm(fmt, a, bs if fmt == NVFP4 else None, ts, 0, fmt, packed, nbytes, 3, 16, 0, y, 16, q.QG_OUT_F32)
+        torch.cuda.synchronize()
+        assert torch.count_nonzero(y) == 0
+    # m = 0: nothing written, no error
+    wq = q.quantize(to_dev_bf16(synth.normal_bf16(16, 128, 0.02, 1, 1)), FP8)
+    packed = q.pack(wq)
+    empty = q.QTensor(FP8, torch.zeros((0, 128), dtype=torch.uint8, device=DEV), None,
+                      torch.ones(1, device=DEV), 0, 128)
+    y = q.linear(empty, packed, FP8, 16)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 16)
+
+
+# ---------------------------------------------------------------- workload sizes
+def _sample(m, n, count, seed):
+    rng = np.random.default_rng(seed)
+    rows = np.concatenate([[0, m - 1, 0, m - 1], rng.integers(0, m, count)])
+    cols = np.concatenate([[0, 0, n - 1, n - 1], rng.integers(0, n, count)])
+    return rows, cols
+
+
+def test_single_fp8_linear_full():
+    x = synth.normal_bf16(128, 256, 1.0, 0, 0)
+    w = synth.normal_bf16(256, 256, 0.02, 0, 1)
+    y = run_linear("fp8", x, w)
+    log("fp8 128x256x256 max err/B", check_linear(y, oracle.linear_reference("fp8", x, w)))
+
+
+def test_single_nvfp4_linear_full():
+    x = synth.normal_bf16(512, 3072, 1.0, 0, 0)
+    w = synth.normal_bf16(3072, 3072, 0.02, 0, 1)
+    y = run_linear("nvfp4", x, w)
+    log("nvfp4 512x3072x3072 max err/B", check_linear(y, oracle.linear_reference("nvfp4", x, w)))
+
+
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4"])
+@pytest.mark.parametrize("name", list(synth.DIT_LINEARS))
+def test_dit_linear_sampled(kind, name):
+    n, k = synth.DIT_LINEARS[name]
+    m = synth.DIT_TOKENS
+    log("dit %s %s m=%d n=%d k=%d" % (kind, name, m, n, k))
+    tail = 0.001 if kind == "nvfp4" else 0.0
+    x = synth.normal_bf16(m, k, 1.0, 0, 0, outlier_frac=tail, outlier_gain=50.0)
+    w = synth.normal_bf16(n, k, 0.02, 0, 1)
+    y = run_linear(kind, x, w)
+    rows, cols = _sample(m, n, 3000, 1)
+    ref = oracle.linear_reference(kind, x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))
+
+
+@pytest.mark.parametrize("name", list(synth.ENCODER_LINEARS))
+@pytest.mark.parametrize("m", synth.ENCODER_TOKENS)
+def test_w4a16_encoder_full(name, m):
+    n, k = synth.ENCODER_LINEARS[name]
+    x = synth.normal_bf16(m, k, 1.0, 0, 0)
+    w = synth.normal_bf16(n, k, 0.02, 0, 1)
+    y = run_linear("w4a16", x, w)
+    log("w4a16 %s m=%d max err/B" % (name, m), check_linear(y, oracle.linear_reference("w4a16", x, w)))

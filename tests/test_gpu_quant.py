@@ -1,0 +1,154 @@
+"""GPU parity of the quantizers, dequantizers and weight packer with the CPU
+oracle: every code, block scale and tensor-scale bit must match."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_21849_amd as q
+import synth
+from gpu_util import DEV, assert_quant_equal, host, log, scale_of, to_dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+FP8, NVFP4 = q.QG_FMT_FP8_E4M3, q.QG_FMT_NVFP4
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+# (rows, cols, sigma, heavy_tail): workload operands plus small and ragged cases
+SHAPES = [
+    (1, 16, 1.0, False), (3, 48, 1.0, False), (37, 160, 1.0, False),
+    (128, 256, 1.0, False), (256, 256, 0.02, False),          # single FP8 linear
+    (512, 3072, 1.0, False), (3072, 3072, 0.02, False),        # single NVFP4 linear
+    (4608, 3072, 1.0, False), (4608, 3072, 1.0, True),          # DiT activations (K = 3072)
+    (4608, 9216, 1.0, True), (9216, 3072, 0.02, False),         # DiT down-proj input, QKV weight
+    (3072, 9216, 0.02, False), (16, 1024, 1.0, False),          # down-proj weight, encoder tokens
+]
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("rows,cols,sigma,tail", SHAPES)
+def test_quantize_bit_exact(fmt, rows, cols, sigma, tail):
+    log("quantize fmt=%d shape=%dx%d tail=%s" % (fmt, rows, cols, tail))
+    x = synth.normal_bf16(rows, cols, sigma, 0, 0, outlier_frac=0.001 if tail else 0.0, outlier_gain=50.0)
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+
+
+@pytest.mark.parametrize("rows,cols", [(5, 37), (2, 7), (1, 1), (9, 130)])
+def test_fp8_ragged_columns(rows, cols):
+    x = synth.normal_bf16(rows, cols, 1.0, 3, 0)
+    qt = q.quantize(to_dev_bf16(x), FP8)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_row_stride_larger_than_row(fmt):
+    full = synth.normal_bf16(64, 400, 1.0, 4, 0)
+    xd = to_dev_bf16(full)[:, :320]
+    assert xd.stride(0) == 400
+    qt = q.quantize(xd, fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, np.ascontiguousarray(full[:, :320]))
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_odd_row_stride_unaligned(fmt):
+    """ldx not a multiple of 8 and a 2-byte-aligned base: the scalar load path."""
+    full = synth.normal_bf16(33, 163, 1.0, 5, 0)
+    xd = to_dev_bf16(full)[:, 1:161]
+    qt = q.quantize(xd, fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, np.ascontiguousarray(full[:, 1:161]))
+
+
+def test_worked_examples():
+    g = json.load(open(GOLDEN))
+    x8 = synth.f32_to_bf16_bits(np.array(g["fp8"]["x"], np.float32))[None, :]
+    q8 = q.quantize(to_dev_bf16(x8), FP8)
+    x4 = synth.f32_to_bf16_bits(np.array(g["nvfp4"]["x"], np.float32))[None, :]
+    q4 = q.quantize(to_dev_bf16(x4), NVFP4)
+    torch.cuda.synchronize()
+    assert host(q8.codes)[0].tolist() == g["fp8"]["codes"]
+    assert scale_of(q8.tensor_scale) == np.float32(g["fp8"]["scale"])
+    c = host(q4.codes)[0]
+    codes = np.stack([c & 15, c >> 4], axis=1).reshape(-1).tolist()
+    assert codes == g["nvfp4"]["element_codes"]
+    assert host(q4.block_scales)[0].tolist() == g["nvfp4"]["block_scales"]
+    assert scale_of(q4.tensor_scale) == np.float32(g["nvfp4"]["tensor_scale"])
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_zero_tensor_and_empty(fmt):
+    x = np.zeros((8, 64), np.uint16)
+    x[3, 5] = 0x8000
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+    e = q.quantize(torch.empty((0, 64), dtype=torch.bfloat16, device=DEV), fmt)
+    torch.cuda.synchronize()
+    assert scale_of(e.tensor_scale) == 0.0
+
+
+def test_tiny_blocks_get_subnormal_scales():
+    """Rows scaled down by 2^-12 .. 2^-20 give E4M3-subnormal and zero block scales."""
+    x = synth.normal_bf16(32, 256, 1.0, 6, 0)
+    xf = synth.bf16_bits_to_f32(x).astype(np.float64)
+    xf[8:] *= 2.0 ** -np.arange(12, 36)[:, None]
+    xb = synth.f32_to_bf16_bits(xf.astype(np.float32))
+    _, bs, _ = oracle.quantize_nvfp4(xb)
+    assert (bs < 8).any() and (bs == 0).any()
+    for fmt in (FP8, NVFP4):
+        qt = q.quantize(to_dev_bf16(xb), fmt)
+        torch.cuda.synchronize()
+        assert_quant_equal(qt, xb)
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_nonfinite_input_gives_nan_scale(fmt):
+    x = synth.normal_bf16(4, 64, 1.0, 7, 0)
+    x[2, 9] = 0x7F80  # +inf
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert np.isnan(scale_of(qt.tensor_scale))
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("out", [q.QG_OUT_F32, q.QG_OUT_BF16])
+def test_dequant_bit_exact(fmt, out):
+    x = synth.normal_bf16(96, 512, 1.0, 8, 0, outlier_frac=0.01, outlier_gain=50.0)
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    d = q.dequantize(qt, out)
+    torch.cuda.synchronize()
+    kind = "f32" if out == q.QG_OUT_F32 else "bf16"
+    if fmt == FP8:
+        c, s = oracle.quantize_fp8(x)
+        ref = oracle.dequant_fp8(c, s, out=kind)
+    else:
+        c, b, s = oracle.quantize_nvfp4(x)
+        ref = oracle.dequant_nvfp4(c, b, s, out=kind)
+    got = host(d) if out == q.QG_OUT_F32 else host(d.view(torch.int16)).view(np.uint16)
+    assert got.dtype == ref.dtype
+    assert np.array_equal(got.view(np.uint32 if out == q.QG_OUT_F32 else np.uint16),
+                          ref.view(np.uint32 if out == q.QG_OUT_F32 else np.uint16))
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("n,k", [(16, 128), (48, 384), (3072, 1024), (1024, 3072)])
+def test_pack_unpack_roundtrip(fmt, n, k):
+    w = synth.normal_bf16(n, k, 0.02, 9, 1)
+    wq = q.quantize(to_dev_bf16(w), fmt)
+    packed = q.pack(wq)
+    back = q.unpack(packed, fmt, n, k)
+    torch.cuda.synchronize()
+    assert torch.equal(back.codes, wq.codes)
+    if fmt == NVFP4:
+        assert torch.equal(back.block_scales, wq.block_scales)
+    assert torch.equal(back.tensor_scale, wq.tensor_scale)
+    # the packed image is a permutation: same multiset of code bytes
+    body = host(packed)[256:256 + host(wq.codes).size]
+    assert np.array_equal(np.sort(body), np.sort(host(wq.codes).reshape(-1)))

@@ -1,0 +1,305 @@
+"""Benchmark of the quantized-linear hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of seeded synthetic
+input shaped like the paper's workloads:
+  * denoising-transformer block linears at a 1024^2 image (M = 4608 tokens,
+    hidden 3072): QKV 3072->9216, attention-out 3072->3072, MLP-up
+    3072->9216, MLP-down 9216->3072, each = run-time activation quantize +
+    quantized GEMM, once in FP8 W8A8 and once in NVFP4 W4A4 (the NVFP4 pass
+    uses heavy-tailed activations: 0.1 % of input channels x50);
+  * the small text encoder's linears 1024->3072 and 3072->1024 with NVFP4
+    weights and bf16 activations (W4A16) at M = 1, 16, 256, 512 tokens.
+Weights are quantized and packed once before timing (offline PTQ). Inputs
+are resident in HBM when the timed region starts.
+
+Prints ONE JSON line (the driver's contract) with the aggregate quantized
+GEMM throughput of the step, a per-part breakdown, a roofline entry for the
+dominant kernel (per-launch HIP events on the launch stream) and the CPU
+oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "quantized GEMM TFLOP/s (FP8, NVFP4) at DiT shapes + % MFMA peak; W4A16 HBM GB/s"
+PEAK = {"fp8": 5000.0, "f16": 2500.0, "bf16": 2500.0, "fp4": 10100.0, "hbm_gbs": 8000.0}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU work for the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pool-mib", type=int, default=600,
+                    help="size of the weight pool for the cold-HBM W4A16 measurement")
+    return ap.parse_args()
+
+
+def dev_bf16(bits):
+    import torch
+    return torch.from_numpy(np.array(bits, dtype=np.uint16, copy=True).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_21849_amd as q
+    import synth
+
+    q.lib()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    t_setup = time.time()
+
+    # ------------------------------------------------------------ inputs and offline weights
+    M = synth.DIT_TOKENS
+    dit = []
+    for li, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
+        base = 16 * li
+        xn = synth.normal_f64(0, base + synth.STREAM_X, M * k).reshape(M, k)
+        x_fp8 = synth.f32_to_bf16_bits((xn * synth.SIGMA_X).astype(np.float32))
+        ch = synth.outlier_channels(0, base + synth.STREAM_OUTLIER, k, synth.HEAVY_TAIL_FRAC)
+        xn[:, ch] *= synth.HEAVY_TAIL_GAIN
+        x_nv = synth.f32_to_bf16_bits((xn * synth.SIGMA_X).astype(np.float32))
+        del xn
+        w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
+        wd = dev_bf16(w)
+        ent = {"name": name, "n": n, "k": k, "x": {"fp8": dev_bf16(x_fp8), "nvfp4": dev_bf16(x_nv)}}
+        for kind, fmt in (("fp8", q.QG_FMT_FP8_E4M3), ("nvfp4", q.QG_FMT_NVFP4)):
+            ent["w_" + kind] = q.pack(q.quantize(wd, fmt))
+            # activation code buffers and output, allocated once
+            if fmt == q.QG_FMT_FP8_E4M3:
+                codes, bs = torch.empty((M, k), dtype=torch.uint8, device="cuda"), None
+            else:
+                codes = torch.empty((M, k // 2), dtype=torch.uint8, device="cuda")
+                bs = torch.empty((M, k // 16), dtype=torch.uint8, device="cuda")
+            ent["a_" + kind] = q.QTensor(fmt, codes, bs, torch.empty(1, device="cuda"), M, k)
+            ent["y_" + kind] = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
+        dit.append(ent)
+        del wd
+    enc = []
+    for ei, (name, (n, k)) in enumerate(synth.ENCODER_LINEARS.items()):
+        base = 64 + 16 * ei
+        w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
+        packed = q.pack(q.quantize(dev_bf16(w), q.QG_FMT_NVFP4))
+        for m in synth.ENCODER_TOKENS:
+            x = dev_bf16(synth.normal_bf16(m, k, synth.SIGMA_X, 0, base + synth.STREAM_X + 100 * m))
+            enc.append({"name": name, "n": n, "k": k, "m": m, "x": x, "w": packed,
+                        "y": torch.empty((m, n), dtype=torch.bfloat16, device="cuda")})
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+
+    # ------------------------------------------------------------ the step as a flat launch list
+    # (integer pointers and a fixed stream handle keep per-launch host overhead small)
+    lib = q.lib()
+    st = torch.cuda.current_stream().cuda_stream
+    plan = []
+    for kind, fmt in (("fp8", q.QG_FMT_FP8_E4M3), ("nvfp4", q.QG_FMT_NVFP4)):
+        for e in dit:
+            a, x, wp, y = e["a_" + kind], e["x"][kind], e["w_" + kind], e["y_" + kind]
+            bs = a.block_scales.data_ptr() if a.block_scales is not None else None
+            plan.append((("quant", kind, e["name"]), lib.qg_quantize_act,
+                         (fmt, x.data_ptr(), M, e["k"], e["k"], a.codes.data_ptr(), bs,
+                          a.tensor_scale.data_ptr(), st)))
+            plan.append((("gemm", kind, e["name"]), lib.qg_gemm,
+                         (fmt, a.codes.data_ptr(), bs, a.tensor_scale.data_ptr(), e["k"], fmt,
+                          wp.data_ptr(), wp.numel(), M, e["n"], e["k"], y.data_ptr(), e["n"],
+                          q.QG_OUT_BF16, st)))
+    for e in enc:
+        plan.append((("gemm", "w4a16", "%s_m%d" % (e["name"], e["m"])), lib.qg_gemm,
+                     (q.QG_FMT_BF16, e["x"].data_ptr(), None, None, e["k"], q.QG_FMT_NVFP4,
+                      e["w"].data_ptr(), e["w"].numel(), e["m"], e["n"], e["k"], e["y"].data_ptr(),
+                      e["n"], q.QG_OUT_BF16, st)))
+
+    def make_events(n):
+        return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+
+    def step(events):
+        for (key, fn, fargs), (s, e) in zip(plan, events):
+            s.record()
+            rc = fn(*fargs)
+            e.record()
+            if rc != 0:
+                raise q.QGError(rc, str(key))
+
+    warm_ev = make_events(len(plan))
+    for _ in range(args.warmup):
+        step(warm_ev)
+    torch.cuda.synchronize()
+    step_events = [make_events(len(plan)) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.time()
+    t0.record()
+    for i in range(args.steps):
+        step(step_events[i])
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.time() - wall0
+    step_ms = t0.elapsed_time(t1) / args.steps
+
+    durations = {}  # per-launch durations (ms) of every launch in the timed steps
+    for evs in step_events:
+        for (key, _, _), (s, e) in zip(plan, evs):
+            durations.setdefault(key, []).append(s.elapsed_time(e))
+
+    # ------------------------------------------------------------ accounting
+    def flops(e, m=M):
+        return 2.0 * m * e["n"] * e["k"]
+
+    parts = {}
+    total_flops = 0.0
+    for kind in ("fp8", "nvfp4"):
+        gemm_ms = sum(np.mean(durations.get(("gemm", kind, e["name"]))) for e in dit)
+        quant_ms = sum(np.mean(durations.get(("quant", kind, e["name"]))) for e in dit)
+        f = sum(flops(e) for e in dit)
+        total_flops += f
+        # algorithmic bytes of the activation quantizer: read 2 B/elem, write codes (+ scales)
+        qbytes = sum(M * e["k"] * (2 + (1.0 if kind == "fp8" else 0.5625)) for e in dit)
+        per = {e["name"]: {"gemm_us": round(1e3 * float(np.mean(durations.get(("gemm", kind, e["name"])))), 2),
+                           "quant_us": round(1e3 * float(np.mean(durations.get(("quant", kind, e["name"])))), 2),
+                           "gemm_tflops": round(flops(e) / (1e9 * float(np.mean(durations.get(("gemm", kind, e["name"]))))), 1)}
+               for e in dit}
+        parts[kind] = {
+            "gemm_tflops": round(f / (gemm_ms * 1e9), 1),
+            "linear_tflops_incl_quant": round(f / ((gemm_ms + quant_ms) * 1e9), 1),
+            "gemm_frac_of_%s_peak" % kind: round(f / (gemm_ms * 1e9) / PEAK["fp8" if kind == "fp8" else "fp4"], 4),
+            "quant_gbs": round(qbytes / (quant_ms * 1e6), 1),
+            "per_linear": per,
+        }
+        if kind == "nvfp4":
+            parts[kind]["gemm_frac_of_f16_mfma_peak"] = round(f / (gemm_ms * 1e9) / PEAK["f16"], 4)
+    w4 = {}
+    for e in enc:
+        key = "%s_m%d" % (e["name"], e["m"])
+        ms = float(np.mean(durations.get(("gemm", "w4a16", key))))
+        byt = e["n"] * e["k"] * 0.5625 + e["m"] * e["k"] * 2 + e["m"] * e["n"] * 2
+        total_flops += flops(e, e["m"])
+        w4[key] = {"us": round(ms * 1e3, 2), "gbs": round(byt / (ms * 1e6), 1),
+                   "tflops": round(flops(e, e["m"]) / (ms * 1e9), 2)}
+    parts["w4a16_single_call"] = w4
+    parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
+    parts["w4a16_cold_pool"] = w4a16_pool(q, synth, args.pool_mib)
+
+    # dominant kernel: the GEMM kind with the largest share of the step
+    shares = {kind: sum(sum(durations.get(("gemm", kind, e["name"]))) for e in dit) for kind in ("fp8", "nvfp4")}
+    dom = max(shares, key=shares.get)
+    launches = [(flops(e), d) for e in dit for d in durations.get(("gemm", dom, e["name"]))]
+    fl = sum(a for a, _ in launches)
+    dur_ms = sum(d for _, d in launches)
+    achieved = fl / (dur_ms * 1e9)  # TFLOP/s
+    peak = PEAK["fp8"] if dom == "fp8" else PEAK["f16"]
+    roofline = {"bound": "mfma", "kernel": "k_gemm<%s>" % ("W8A8 fp8 MFMA" if dom == "fp8" else "W4A4 fp16 MFMA"),
+                "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": None,
+                "avg_launch_us": round(1e3 * dur_ms / len(launches), 2), "launches": len(launches),
+                "flops_per_launch_avg": fl / len(launches)}
+
+    value = total_flops / (step_ms * 1e9)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8(e4m3)+fp16(nvfp4 exact dequant)+bf16(w4a16)", "data": "synthetic",
+        "config": {"workload": "DiT block linears at 1024^2 (M=4608; QKV 3072->9216, attn-out 3072->3072, "
+                               "MLP-up 3072->9216, MLP-down 9216->3072) as FP8 W8A8 and NVFP4 W4A4 with "
+                               "run-time activation quantization, + W4A16 text-encoder linears "
+                               "1024<->3072 at M in {1,16,256,512}",
+                   "tokens": M, "seed": 0},
+        "roofline": roofline,
+        "parts": parts,
+        "setup_s": round(t_setup, 1),
+        "timed_wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def w4a16_pool(q, synth, pool_mib):
+    """Cold-HBM W4A16: M in {1, 16} against a pool of distinct encoder weights
+    stacked along N (one call streams the whole pool once; pool > 2x the
+    256 MB last-level cache)."""
+    import torch
+    n1, k1 = synth.ENCODER_LINEARS["down"]            # 1024 x 3072 per weight
+    per = n1 * k1 * 0.5625
+    layers = max(1, int(pool_mib * 2 ** 20 // per))
+    n = layers * n1
+    # quantize the pool from one seeded bf16 weight per 64 layers (tiled) to keep setup short
+    w = synth.normal_bf16(64 * n1, k1, synth.SIGMA_W, 0, 200)
+    wd = torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).cuda()
+    reps = (layers + 63) // 64
+    wd = wd.repeat(reps, 1)[:n].contiguous()
+    packed = q.pack(q.quantize(wd, q.QG_FMT_NVFP4))
+    del wd
+    res = {"layers": layers, "pool_mb": round(packed.numel() / 1e6, 1)}
+    for m in (1, 16):
+        x = dev_bf16(synth.normal_bf16(m, k1, synth.SIGMA_X, 0, 300 + m))
+        y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+        fn = lambda: q.qg_gemm(q.QG_FMT_BF16, x, None, None, k1, q.QG_FMT_NVFP4, packed, packed.numel(),
+                               m, n, k1, y, n, q.QG_OUT_BF16)
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps_t = 10
+        s.record()
+        for _ in range(reps_t):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / reps_t
+        byt = n * k1 * 0.5625 + m * k1 * 2 + m * n * 2
+        res["m%d" % m] = {"us": round(ms * 1e3, 1), "gbs": round(byt / (ms * 1e6), 1),
+                          "frac_of_hbm_peak": round(byt / (ms * 1e6) / PEAK["hbm_gbs"], 4)}
+    del packed
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(target_s: float):
+    """The CPU oracle (as it stands) on a bounded sample of the same workload:
+    NVFP4 quantization of a slice of the QKV activations plus the fp64
+    product of that slice with the quantized QKV weight."""
+    import oracle
+    import synth
+    n, k = synth.DIT_LINEARS["qkv"]
+    w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, synth.STREAM_W)
+    qw, bw, sw = oracle.quantize_nvfp4(w)
+    wdeq = oracle.dequant_nvfp4(qw, bw, sw)
+    rows_done, t_spent, flops = 0, 0.0, 0.0
+    chunk = 8
+    while t_spent < target_s and rows_done < 4608:
+        x = synth.normal_bf16(chunk, k, 1.0, 0, 1000 + rows_done)
+        t0 = time.time()
+        qa, ba, sa = oracle.quantize_nvfp4(x)
+        a = oracle.dequant_nvfp4(qa, ba, sa)
+        oracle.gemm_f64(a, wdeq)
+        t_spent += time.time() - t0
+        rows_done += chunk
+        flops += 2.0 * chunk * n * k
+    return {"value": round(flops / t_spent / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(t_spent, 2),
+            "sample": "NVFP4 W4A4 QKV linear (N=9216, K=3072): %d of 4608 token rows, activation "
+                      "quantize + dequant + fp64 product; weight quantized offline" % rows_done}
+
+
+if __name__ == "__main__":
+    main()

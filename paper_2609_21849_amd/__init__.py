@@ -167,7 +167,8 @@ def quantize(x, fmt: int, stream=None) -> QTensor:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
         bs = torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev)
     ts = torch.empty(1, dtype=torch.float32, device=dev)
-    qg_quantize_act(fmt, x, rows, cols, x.stride(0), codes, bs, ts, stream)
+    ldx = x.stride(0) if rows > 1 else cols   # a size-1 dimension may carry any stride
+    qg_quantize_act(fmt, x, rows, cols, ldx, codes, bs, ts, stream)
     return QTensor(fmt, codes, bs, ts, rows, cols)
 
 
@@ -204,11 +205,13 @@ def linear(a, w_packed, w_fmt: int, n: int, out_dtype: int = QG_OUT_BF16, y=None
         dev = a.codes.device
     else:
         m, k = a.shape
-        a_fmt, a_data, a_bs, a_ts, lda = QG_FMT_BF16, a, None, None, a.stride(0)
+        a_fmt, a_data, a_bs, a_ts = QG_FMT_BF16, a, None, None
+        lda = a.stride(0) if m > 1 else k
         dev = a.device
     if y is None:
         y = torch.empty((m, n), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16, device=dev)
-    qg_gemm(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, y, y.stride(0), out_dtype, stream)
+    ldy = y.stride(0) if m > 1 else n
+    qg_gemm(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, y, ldy, out_dtype, stream)
     return y
 
 

@@ -46,23 +46,47 @@ def test_small_full_parity(kind, m, n, k, out):
     check_linear(y, ref)
 
 
+E2M1_VALUES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def _exact_operand(rows, k, kind, rng, one_hot):
+    """Values the format represents exactly with power-of-two tensor scales.
+
+    FP8   : amax 1.75 (activations) or 7 (weights) -> s = 2^-8 / 2^-6, and every
+            value times 1/s is an E4M3 value.
+    NVFP4 : every 16-block holds +-5.25 and otherwise E2M1 values times 0.875;
+            a_t = 5.25 = 2688 * 2^-9 -> s_t = 2^-9, each block scale is 448.
+    """
+    v = np.zeros((rows, k))
+    if kind == "fp8":
+        if one_hot:
+            for i in range(rows):
+                for b in range(k // 16):
+                    v[i, 16 * b + rng.integers(16)] = rng.choice([-1.75, 1.75])
+        else:
+            v = rng.integers(-7, 8, size=(rows, k)).astype(np.float64)
+            v[:, 0] = 7.0
+    else:
+        for i in range(rows):
+            for b in range(k // 16):
+                if not one_hot:
+                    v[i, 16 * b:16 * b + 16] = rng.choice(E2M1_VALUES, 16) * rng.choice([-1, 1], 16) * 0.875
+                v[i, 16 * b + rng.integers(16)] = rng.choice([-5.25, 5.25])
+    x = synth.f32_to_bf16_bits(v.astype(np.float32))
+    assert np.array_equal(synth.bf16_bits_to_f32(x), v.astype(np.float32))
+    return x
+
+
 @pytest.mark.parametrize("kind", ["fp8", "nvfp4", "w4a16"])
-def test_structured_one_hot(kind):
-    """X = rows of +-1 at one position per 16-block, W = small integers: every
-    dequantized product is exact and the fp32 output must be exact too
-    (catches any transposition of the matrix-core operand or output layout)."""
+def test_structured_exact(kind):
+    """Operands whose quantization is exact and whose tensor scales are powers
+    of two; X has one nonzero per 16-block. Every product and partial sum is
+    exact in fp32, so the fp32 output must equal the oracle bit for bit
+    (catches any transposition or shuffle of operand or output layouts)."""
     m, n, k = 48, 64, 256
     rng = np.random.default_rng(12)
-    xf = np.zeros((m, k), np.float32)
-    for i in range(m):
-        for b in range(k // 16):
-            xf[i, 16 * b + rng.integers(16)] = rng.choice([-1.0, 1.0]) * 4.0
-    wf = rng.integers(-6, 7, size=(n, k)).astype(np.float32)
-    wf[:, 0] = 6.0  # amax 6 in every weight row/block keeps scales powers of two
-    for b in range(k // 16):
-        wf[:, 16 * b] = 6.0
-    x = synth.f32_to_bf16_bits(xf)
-    w = synth.f32_to_bf16_bits(wf)
+    x = _exact_operand(m, k, "fp8" if kind == "fp8" else "nvfp4", rng, one_hot=True)
+    w = _exact_operand(n, k, "fp8" if kind == "fp8" else "nvfp4", rng, one_hot=False)
     y = run_linear(kind, x, w, q.QG_OUT_F32)
     ref = oracle.linear_reference(kind, x, w)
     got = host(y).astype(np.float64)

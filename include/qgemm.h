@@ -81,9 +81,11 @@ typedef enum qg_out_dtype {
  *   x             bf16 [rows, ldx], the first `cols` of each row are used.
  *   codes         out: FP8 [rows, cols] bytes; NVFP4 [rows, cols/2] bytes.
  *   block_scales  out: NVFP4 [rows, cols/16] E4M3 bytes; must be NULL for FP8.
- *   tensor_scale  out: one fp32 decode scale. It doubles as the scratch slot
- *                 of the tensor-wide max reduction, so it must not alias
- *                 the other buffers.
+ *   tensor_scale  out: one fp32 decode scale.
+ *   The tensor-wide max is reduced in two kernels whose partial results are
+ *   parked in `codes` (overwritten by the codes afterwards) or, for tensors
+ *   of a few elements, in `tensor_scale`; so x, codes, block_scales and
+ *   tensor_scale must not overlap.
  *
  * Arithmetic (bit-exact; every step one IEEE binary32 operation, RNE):
  *   FP8  : a = max|x|; s = a/448; r = s>0 ? 1/s : 0; q = E4M3(x*r)

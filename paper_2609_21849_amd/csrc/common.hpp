@@ -16,6 +16,7 @@ namespace qg {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
@@ -106,6 +107,36 @@ __host__ __device__ inline _Float16 e4m3_to_f16(uint32_t c) {
   uint32_t h = (mag >= 8u) ? ((mag << 7) + (8u << 10)) : sub;
   h |= (c & 0x80u) << 8;
   return __builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+// ---------------------------------------------------------------------------
+// Hardware conversions used by the quantizers (gfx950). Both are checked on
+// the GPU against the integer encoders above over all 2^32 fp32 inputs:
+//   E2M1: v_cvt_scalef32_pk_fp4_f32 with scale 1.0 equals enc_e2m1 on every
+//         input (RNE, ties to even code, saturation at 6, sign of zero).
+//   E4M3: v_cvt_scalef32_pk_fp8_f32 with scale 1.0 turns magnitudes above
+//         464 into NaN instead of saturating; after a clamp to [-448, 448]
+//         (v_med3_f32, which keeps -0) it equals enc_e4m3 on every finite input.
+// Element 2i / the first operand lands in the low nibble / low byte.
+__device__ inline uint32_t hw_e2m1x8(const float* y) {
+  uint32_t w = 0;
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[0], y[1], 1.0f, 0);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[2], y[3], 1.0f, 1);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[4], y[5], 1.0f, 2);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[6], y[7], 1.0f, 3);
+  return w;
+}
+
+__device__ inline uint32_t hw_e4m3x4(const float* y) {
+  typedef short v2s __attribute__((ext_vector_type(2)));
+  v2s w = {0, 0};
+  const float a = __builtin_amdgcn_fmed3f(y[0], -448.0f, 448.0f);
+  const float b = __builtin_amdgcn_fmed3f(y[1], -448.0f, 448.0f);
+  const float c = __builtin_amdgcn_fmed3f(y[2], -448.0f, 448.0f);
+  const float d = __builtin_amdgcn_fmed3f(y[3], -448.0f, 448.0f);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, a, b, 1.0f, false);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, c, d, 1.0f, true);
+  return __builtin_bit_cast(uint32_t, w);
 }
 
 }  // namespace qg

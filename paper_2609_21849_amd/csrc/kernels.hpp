@@ -14,16 +14,20 @@ namespace qg {
 // NVFP4) the block-scale region. Header fields (little endian):
 //   +0 u32 magic 'QGPW', +4 u32 layout version, +8 u32 format,
 //   +16 i64 n, +24 i64 k, +32 f32 tensor decode scale.
+// The weight is stored in panels of 32 rows (n rounded up to a multiple of
+// 32, padding rows are zero codes) and chunks of 128 reduction elements.
 constexpr uint32_t kPackMagic = 0x57504751u;  // "QGPW"
-constexpr uint32_t kPackVersion = 1u;
+constexpr uint32_t kPackVersion = 2u;
 constexpr int64_t kPackHeader = 256;
 constexpr int64_t kPackScaleOffset = 32;
+constexpr int64_t kPanel = 32;
 
+inline int64_t padded_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPanel; }
 inline int64_t packed_codes_bytes(int fmt, int64_t n, int64_t k) {
-  return fmt == 1 ? n * k : n * k / 2;
+  return fmt == 1 ? padded_rows(n) * k : padded_rows(n) * k / 2;
 }
 inline int64_t packed_total_bytes(int fmt, int64_t n, int64_t k) {
-  return kPackHeader + packed_codes_bytes(fmt, n, k) + (fmt == 2 ? n * k / 16 : 0);
+  return kPackHeader + packed_codes_bytes(fmt, n, k) + (fmt == 2 ? padded_rows(n) * k / 16 : 0);
 }
 
 hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,

@@ -1,17 +1,17 @@
 // pack.hip -- offline weight re-layout into matrix-core operand order.
 //
 // PTQ weights are quantized once (Sec. 4, quantization paragraph) and then
-// laid out so that the GEMM streams them with no index arithmetic: the
-// weight [n, k] is cut into panels of 16 rows, each panel into chunks of
-// 128 reduction elements, and a chunk is stored in the order the 64 lanes
-// of a wavefront hold it as an MFMA operand. Lane l owns row (l % 16) of
-// the panel and the 32 consecutive reduction elements starting at
-// 32 * (l / 16) of the chunk:
-//   FP8  : 2048-byte chunk; 16-byte piece h (h = 0, 1) of lane l at
-//          h * 1024 + 16 * l, so each half of the operand is one
-//          contiguous 1 KiB wave load.
-//   NVFP4: 1024-byte code chunk, lane l's 16 bytes at 16 * l; block scales
-//          in a separate region, 128 bytes per chunk = [row][8 blocks].
+// laid out so that the GEMM streams them with no index arithmetic. The
+// weight [n, k] is cut into panels of 32 rows (n rounded up to 32 with zero
+// rows) and each panel into chunks of 128 reduction elements. Inside a chunk
+// the 64 lanes of a wavefront each own one row r = l % 32 and one contiguous
+// half of the chunk's reduction range, g = l / 32 -- the operand order of the
+// 32x32 MFMAs once the reduction index is permuted the same way for both
+// operands. A lane's bytes are split into 16-byte pieces h, stored as
+// [h][lane][16 B], so that each piece is one contiguous 1 KiB wave access:
+//   FP8  : 4096-byte chunk, piece h of lane l = row r, bytes 64 g + 16 h;
+//   NVFP4: 2048-byte code chunk, piece h of lane l = row r, bytes 32 g + 16 h;
+//          block scales in their own region, 256 bytes per chunk = [row][8].
 // Chunks of one panel follow each other along k, so a panel is one
 // contiguous stream. The header keeps format, n, k and the tensor scale.
 #include "common.hpp"
@@ -34,52 +34,54 @@ __global__ void k_unpack_header(const uint8_t* packed, float* tscale) {
   *tscale = reinterpret_cast<const float*>(packed + kPackScaleOffset)[0];
 }
 
-// Byte offset, in the canonical [n, row_bytes] code matrix, of the 16-byte
-// piece that packed piece `p` holds (see the layout above).
-__device__ inline int64_t canon_piece(int fmt, int64_t p, int64_t k) {
+// Canonical [n, row_bytes] byte offset of the 16-byte piece that packed
+// piece `p` holds, or -1 for a padding row (see the layout above).
+__device__ inline int64_t canon_piece(int fmt, int64_t p, int64_t n, int64_t k) {
   const int64_t kc_n = k / 128;
-  if (fmt == 1) {                                  // 128 pieces per chunk
-    const int64_t chunk = p >> 7, s = p & 127;
-    const int64_t panel = chunk / kc_n, kc = chunk - panel * kc_n;
-    const int64_t h = s >> 6, l = s & 63;
-    return (panel * 16 + (l & 15)) * k + kc * 128 + 32 * (l >> 4) + 16 * h;
-  } else {                                         // 64 pieces per chunk
-    const int64_t chunk = p >> 6, l = p & 63;
-    const int64_t panel = chunk / kc_n, kc = chunk - panel * kc_n;
-    return (panel * 16 + (l & 15)) * (k / 2) + kc * 64 + 16 * (l >> 4);
-  }
+  const int per = (fmt == 1) ? 256 : 128;            // pieces per chunk
+  const int64_t chunk = p / per, s = p - chunk * per;
+  const int64_t panel = chunk / kc_n, kc = chunk - panel * kc_n;
+  const int64_t h = s >> 6, l = s & 63;
+  const int64_t row = panel * 32 + (l & 31);
+  if (row >= n) return -1;
+  if (fmt == 1) return row * k + kc * 128 + 64 * (l >> 5) + 16 * h;
+  return row * (k / 2) + kc * 64 + 32 * (l >> 5) + 16 * h;
 }
 
-// Byte offset, in the canonical [n, k/16] block-scale matrix, of the 8-byte
-// run that packed scale run `p` holds (run = one row of one chunk).
-__device__ inline int64_t canon_scale_run(int64_t p, int64_t k) {
+// Canonical [n, k/16] offset of the 8-byte scale run that packed run `p`
+// holds (run = one row of one chunk), or -1 for a padding row.
+__device__ inline int64_t canon_scale_run(int64_t p, int64_t n, int64_t k) {
   const int64_t kc_n = k / 128;
-  const int64_t chunk = p >> 4, r = p & 15;
+  const int64_t chunk = p >> 5, r = p & 31;
   const int64_t panel = chunk / kc_n, kc = chunk - panel * kc_n;
-  return (panel * 16 + r) * (k / 16) + kc * 8;
+  const int64_t row = panel * 32 + r;
+  if (row >= n) return -1;
+  return row * (k / 16) + kc * 8;
 }
 
 template <bool PACK>
 __global__ void __launch_bounds__(256) k_pack_codes(int fmt, uint8_t* canon, uint8_t* packed_codes,
-                                                    int64_t npieces, int64_t k) {
+                                                    int64_t npieces, int64_t n, int64_t k) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= npieces) return;
-  const int64_t c = canon_piece(fmt, p, k);
+  const int64_t c = canon_piece(fmt, p, n, k);
   if (PACK)
-    reinterpret_cast<uint4*>(packed_codes)[p] = *reinterpret_cast<const uint4*>(canon + c);
-  else
+    reinterpret_cast<uint4*>(packed_codes)[p] =
+        (c < 0) ? make_uint4(0u, 0u, 0u, 0u) : *reinterpret_cast<const uint4*>(canon + c);
+  else if (c >= 0)
     *reinterpret_cast<uint4*>(canon + c) = reinterpret_cast<const uint4*>(packed_codes)[p];
 }
 
 template <bool PACK>
 __global__ void __launch_bounds__(256) k_pack_scales(uint8_t* canon, uint8_t* packed_scales,
-                                                     int64_t nruns, int64_t k) {
+                                                     int64_t nruns, int64_t n, int64_t k) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= nruns) return;
-  const int64_t c = canon_scale_run(p, k);
+  const int64_t c = canon_scale_run(p, n, k);
   if (PACK)
-    reinterpret_cast<uint2*>(packed_scales)[p] = *reinterpret_cast<const uint2*>(canon + c);
-  else
+    reinterpret_cast<uint2*>(packed_scales)[p] =
+        (c < 0) ? make_uint2(0u, 0u) : *reinterpret_cast<const uint2*>(canon + c);
+  else if (c >= 0)
     *reinterpret_cast<uint2*>(canon + c) = reinterpret_cast<const uint2*>(packed_scales)[p];
 }
 
@@ -93,11 +95,11 @@ hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, con
   uint8_t* pc = packed + kPackHeader;
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<true>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt,
-                     const_cast<uint8_t*>(codes), pc, npieces, k);
+                     const_cast<uint8_t*>(codes), pc, npieces, n, k);
   if (fmt == 2) {
-    const int64_t nruns = n * k / 128;
+    const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_scales<true>, dim3(blocks_for(nruns)), dim3(256), 0, st,
-                       const_cast<uint8_t*>(bscale), pc + cb, nruns, k);
+                       const_cast<uint8_t*>(bscale), pc + cb, nruns, n, k);
   }
   return hipGetLastError();
 }
@@ -110,11 +112,11 @@ hipError_t launch_unpack(int fmt, const uint8_t* packed, int64_t n, int64_t k, u
   uint8_t* pc = const_cast<uint8_t*>(packed) + kPackHeader;
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<false>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt, codes,
-                     pc, npieces, k);
+                     pc, npieces, n, k);
   if (fmt == 2) {
-    const int64_t nruns = n * k / 128;
+    const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_scales<false>, dim3(blocks_for(nruns)), dim3(256), 0, st, bscale,
-                       pc + cb, nruns, k);
+                       pc + cb, nruns, n, k);
   }
   return hipGetLastError();
 }

@@ -8,13 +8,12 @@
 //
 // A tensor-wide scale needs the tensor-wide max before any element can be
 // coded, so one call is a short chain on the caller's stream:
-//   k_fill       : zero the fp32 scale slot (a kernel, not a memset, so the
-//                  chain can be captured in a HIP graph)
-//   k_amax       : max |x| as integer max of bf16 magnitude bits, wave
-//                  reduction, one atomicMax per workgroup on the slot (the
-//                  bit pattern of a non-negative float orders like the float)
-//   k_finalize   : slot (amax bits) -> decode scale s or s_t, in place
-//   k_quant_*    : each thread codes 16 elements with the finished scale
+//   k_amax_partial : max |x| as an integer max of bf16 magnitude bits (the
+//                    bit pattern of a non-negative value orders like the
+//                    value); one partial per workgroup, parked in the code
+//                    buffer that the last kernel overwrites anyway
+//   k_finalize     : max of the partials -> decode scale s or s_t
+//   k_quant_*      : code the elements with the finished scale
 // Stream order separates the kernels; nothing waits on the host.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -26,25 +25,42 @@ __global__ void k_fill_u32(uint32_t* p, uint32_t v) { *p = v; }
 // ---------------------------------------------------------------- amax
 // Rows of `cols` bf16 elements, `ldx` apart. VEC: rows are 16-byte aligned
 // and cols % 8 == 0, so each step reads 8 elements with one 16-byte load.
+// Each workgroup writes the bf16 magnitude bits of its max to partial[id];
+// there are no atomics, so thousands of workgroups do not serialise on one
+// address. k_finalize reduces the partials.
 template <bool VEC>
-__global__ void __launch_bounds__(256) k_amax(const uint16_t* __restrict__ x, int64_t rows,
-                                              int64_t cols, int64_t ldx, uint32_t* slot) {
+__global__ void __launch_bounds__(256) k_amax_partial(const uint16_t* __restrict__ x, int64_t rows,
+                                                      int64_t cols, int64_t ldx,
+                                                      uint32_t* __restrict__ partial) {
   uint32_t m = 0;
+  const int64_t stride = (int64_t)gridDim.x * 256;
   for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
     const uint16_t* xr = x + r * ldx;
     if (VEC) {
       const int64_t units = cols >> 3;
-      for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < units;
-           u += (int64_t)gridDim.x * 256) {
-        const uint4 v = *reinterpret_cast<const uint4*>(xr + u * 8);
-        const uint32_t w0 = v.x & 0x7FFF7FFFu, w1 = v.y & 0x7FFF7FFFu;
-        const uint32_t w2 = v.z & 0x7FFF7FFFu, w3 = v.w & 0x7FFF7FFFu;
-        m = max(m, max(max(w0 & 0xFFFFu, w0 >> 16), max(w1 & 0xFFFFu, w1 >> 16)));
-        m = max(m, max(max(w2 & 0xFFFFu, w2 >> 16), max(w3 & 0xFFFFu, w3 >> 16)));
+      const uint4* xv = reinterpret_cast<const uint4*>(xr);
+      int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+      for (; u + 3 * stride < units; u += 4 * stride) {
+        const uint4 v0 = xv[u], v1 = xv[u + stride], v2 = xv[u + 2 * stride], v3 = xv[u + 3 * stride];
+        const uint32_t w[16] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w,
+                          v2.x, v2.y, v2.z, v2.w, v3.x, v3.y, v3.z, v3.w};
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t t = w[i] & 0x7FFF7FFFu;
+          m = max(m, max(t & 0xFFFFu, t >> 16));
+        }
+      }
+      for (; u < units; u += stride) {
+        const uint4 v = xv[u];
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t t = w[i] & 0x7FFF7FFFu;
+          m = max(m, max(t & 0xFFFFu, t >> 16));
+        }
       }
     } else {
-      for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < cols;
-           c += (int64_t)gridDim.x * 256)
+      for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < cols; c += stride)
         m = max(m, (uint32_t)(xr[c] & 0x7FFFu));
     }
   }
@@ -52,18 +68,26 @@ __global__ void __launch_bounds__(256) k_amax(const uint16_t* __restrict__ x, in
   __shared__ uint32_t part[4];
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    m = max(max(part[0], part[1]), max(part[2], part[3]));
-    if (m) atomicMax(slot, m << 16);  // bf16 magnitude bits -> fp32 bits
-  }
+  if (threadIdx.x == 0)
+    partial[blockIdx.y * gridDim.x + blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
 }
 
-// amax bits -> decode scale. divisor = 448 (FP8) or 2688 = 448 * 6 (NVFP4).
-// Inf/NaN anywhere in the tensor leaves a NaN scale as the sentinel.
-__global__ void k_finalize(uint32_t* slot, float divisor) {
-  const uint32_t a = *slot;
-  const float s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), divisor);
-  *reinterpret_cast<float*>(slot) = s;
+// Max of `count` partials (bf16 magnitude bits) -> decode scale, written to
+// `slot`. divisor = 448 (FP8) or 2688 = 448 * 6 (NVFP4). Inf/NaN anywhere in
+// the tensor leaves a NaN scale as the sentinel. `partial` may be `slot`
+// itself (count 1): every read happens before the barrier, the write after.
+__global__ void __launch_bounds__(256) k_finalize(const uint32_t* partial, int count, float* slot,
+                                                  float divisor) {
+  uint32_t m = 0;
+  for (int i = threadIdx.x; i < count; i += 256) m = max(m, partial[i]);
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t a = max(max(part[0], part[1]), max(part[2], part[3])) << 16;
+    *slot = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), divisor);
+  }
 }
 
 // ---------------------------------------------------------------- element access
@@ -166,6 +190,72 @@ __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict_
   bscale[t] = (uint8_t)sb;
 }
 
+// ---------------------------------------------------------------- dense tensors
+// Dense tensors (ldx == cols, 16-byte aligned rows): each wavefront codes a
+// chunk of 1024 consecutive elements. Lane l reads elements [8l, 8l + 8) and
+// [512 + 8l, 512 + 8l + 8) of the chunk with one 16-byte load each, so every
+// load and store instruction of the wave covers one contiguous run of memory.
+// Elements are coded with the hardware conversions (hw_e4m3x4 / hw_e2m1x8).
+// NVFP4: n % 16 == 0, so lanes (2j, 2j+1) hold one whole 16-element block
+// (or both lie past the end); the block max is shared with one lane swap.
+template <int FMT>
+__global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict__ x, int64_t n,
+                                                     uint8_t* __restrict__ q,
+                                                     uint8_t* __restrict__ bscale,
+                                                     const float* __restrict__ tscale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t chunk = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+  const float s = *tscale;
+  const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
+  const float d_t = __fmul_rn(6.0f, s);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int64_t e0 = chunk * 1024 + h * 512 + lane * 8;
+    const bool full = (e0 + 8 <= n);
+    float v[8];
+    if (full) {
+      const uint4 w = *reinterpret_cast<const uint4*>(x + e0);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[2 * j] = bf16_lo(ww[j]);
+        v[2 * j + 1] = bf16_hi(ww[j]);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = (e0 + j < n) ? u2f((uint32_t)x[e0 + j] << 16) : 0.0f;
+    }
+    if (FMT == 1) {
+      float y[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
+      const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
+      if (full) {
+        *reinterpret_cast<uint2*>(q + e0) = make_uint2(lo, hi);
+      } else {
+        for (int j = 0; j < 8 && e0 + j < n; ++j) q[e0 + j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
+      }
+    } else {
+      uint32_t am = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
+      am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+      const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(am), d_t) : 0.0f;
+      const uint32_t sb = enc_e4m3(vb);
+      const float S = __fmul_rn(dec_e4m3(sb), s);
+      const float rb = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
+      float y[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], rb);
+      const uint32_t w = hw_e2m1x8(y);
+      if (full) {
+        *reinterpret_cast<uint32_t*>(q + (e0 >> 1)) = w;
+        if ((lane & 1) == 0) bscale[e0 >> 4] = (uint8_t)sb;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- dequant
 // out = fl(e4m3(q) * s)  or  fl(fl(e2m1(q) * e4m3(s_b)) * s_t), as fp32 or
 // RNE bf16; one thread per 16 consecutive elements of the dense tensor.
@@ -238,35 +328,53 @@ static inline unsigned grid_for(int64_t threads) { return (unsigned)((threads + 
 
 hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
                            uint8_t* codes, uint8_t* bscale, float* tscale, hipStream_t st) {
-  uint32_t* slot = reinterpret_cast<uint32_t*>(tscale);
-  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(1), 0, st, slot, 0u);
-  if (rows == 0 || cols == 0) return hipGetLastError();
+  if (rows == 0 || cols == 0) {
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(1), 0, st, reinterpret_cast<uint32_t*>(tscale), 0u);
+    return hipGetLastError();
+  }
   const bool contig = (ldx == cols);
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0);
-  // amax
+  // amax: per-workgroup partial maxima are parked in the code buffer, which
+  // the quantize kernel overwrites afterwards (stream order separates them).
   {
     const int64_t r_eff = contig ? 1 : rows;
     const int64_t c_eff = contig ? rows * cols : cols;
     const bool vec = aligned && (c_eff % 8 == 0) && (contig || ldx % 8 == 0);
     const int64_t per_row = vec ? c_eff / 8 : c_eff;
-    unsigned gx = (unsigned)std::min<int64_t>(std::max<int64_t>(1, (per_row + 255) / 256), 4096);
-    unsigned gy = (unsigned)std::min<int64_t>(r_eff, 65535);
-    if ((int64_t)gx * gy > 8192) gx = std::max<unsigned>(1u, 8192u / gy);
+    const int64_t code_bytes = (fmt == 1) ? rows * cols : rows * cols / 2;
+    const uintptr_t base = (reinterpret_cast<uintptr_t>(codes) + 3) & ~uintptr_t(3);
+    const int64_t cap = (code_bytes - (int64_t)(base - reinterpret_cast<uintptr_t>(codes))) / 4;
+    int64_t gy = std::min<int64_t>(r_eff, 1024);
+    int64_t gx = std::min<int64_t>(std::max<int64_t>(1, (per_row + 1023) / 1024), std::max<int64_t>(1, 1024 / gy));
+    uint32_t* partial = reinterpret_cast<uint32_t*>(base);
+    if (gx * gy > cap) {   // tiny tensor: one workgroup, its max goes straight to the scale slot
+      gx = gy = 1;
+      partial = reinterpret_cast<uint32_t*>(tscale);
+    }
     if (vec)
-      hipLaunchKernelGGL(k_amax<true>, dim3(gx, gy), dim3(256), 0, st, x, r_eff, c_eff, contig ? c_eff : ldx, slot);
+      hipLaunchKernelGGL(k_amax_partial<true>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
+                         contig ? c_eff : ldx, partial);
     else
-      hipLaunchKernelGGL(k_amax<false>, dim3(gx, gy), dim3(256), 0, st, x, r_eff, c_eff, contig ? c_eff : ldx, slot);
+      hipLaunchKernelGGL(k_amax_partial<false>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
+                         contig ? c_eff : ldx, partial);
+    hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, st, partial, (int)(gx * gy), tscale,
+                       fmt == 1 ? 448.0f : 2688.0f);
   }
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(1), 0, st, slot, fmt == 1 ? 448.0f : 2688.0f);
-  if (fmt == 1) {
-    const bool qal = (reinterpret_cast<uintptr_t>(codes) % 16 == 0);
+  const int64_t n = rows * cols;
+  const bool qal = (reinterpret_cast<uintptr_t>(codes) % 8 == 0);
+  if (contig && aligned && qal) {
+    const unsigned g = (unsigned)((n + 4095) / 4096);  // 4 waves x 1024 elements per workgroup
+    if (fmt == 1) hipLaunchKernelGGL(k_quant_dense<1>, dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+    else hipLaunchKernelGGL(k_quant_dense<2>, dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+  } else if (fmt == 1) {
+    const bool qal16 = (reinterpret_cast<uintptr_t>(codes) % 16 == 0);
     if (contig) {
-      const bool vec = aligned && qal;
+      const bool vec = aligned && qal16;
       const unsigned g = grid_for((rows * cols + 15) / 16);
       if (vec) hipLaunchKernelGGL((k_quant_fp8<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
       else hipLaunchKernelGGL((k_quant_fp8<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
     } else {
-      const bool vec = aligned && qal && (ldx % 8 == 0) && (cols % 16 == 0);
+      const bool vec = aligned && qal16 && (ldx % 8 == 0) && (cols % 16 == 0);
       const unsigned g = grid_for(rows * ((cols + 15) / 16));
       if (vec) hipLaunchKernelGGL((k_quant_fp8<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
       else hipLaunchKernelGGL((k_quant_fp8<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);

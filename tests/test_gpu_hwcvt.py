@@ -1,0 +1,46 @@
+"""The quantizers code elements with gfx950's conversion instructions
+(csrc/common.hpp: hw_e2m1x8, hw_e4m3x4). These tests run those exact device
+functions on all 2^32 fp32 inputs and require them to equal the library's
+integer encoders -- which tests/test_encoder_exhaustive.py ties to the CPU
+oracle on the same 2^32 inputs. The GEMM's W4A4 dequantization relies on
+v_cvt_scalef32_pk_f16_fp4 returning the exact E2M1 values at scale 1.0."""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+LIB = os.path.join(os.path.dirname(__file__), "native", "libqgprobe.so")
+
+
+def _probe():
+    if not os.path.exists(LIB):
+        pytest.fail("tests/native/libqgprobe.so is not built (__graft_entry__.build())")
+    return ctypes.CDLL(LIB)
+
+
+@pytest.mark.parametrize("which,name", [(0, "e2m1"), (1, "e4m3")])
+def test_hw_encoder_equals_integer_encoder_on_all_fp32(which, name):
+    L = _probe()
+    counts = torch.zeros(2, dtype=torch.int64, device="cuda")
+    first = torch.zeros(16, dtype=torch.int32, device="cuda")
+    assert L.qgp_probe_cvt(which, ctypes.c_void_p(counts.data_ptr()), ctypes.c_void_p(first.data_ptr())) == 0
+    torch.cuda.synchronize()
+    c = counts.cpu().tolist()
+    f = first.cpu().numpy().view(np.uint32)
+    print(name, "mismatches (all, finite):", c, [hex(v) for v in f[:8]], flush=True)
+    assert c[1] == 0, "finite mismatches %d, e.g. inputs %s -> hw %s" % (c[1], [hex(v) for v in f[:4]], [hex(v) for v in f[8:12]])
+
+
+def test_f16_conversion_of_e2m1_is_exact_at_unit_scale():
+    L = _probe()
+    out = torch.zeros(8192, dtype=torch.int16, device="cuda")
+    assert L.qgp_probe_f16_scale(ctypes.c_void_p(out.data_ptr())) == 0
+    torch.cuda.synchronize()
+    o = out.cpu().numpy().view(np.float16).astype(np.float64).reshape(256, 16, 2)
+    assert np.array_equal(o[:, :, 0], np.broadcast_to(oracle.e2m1_table(), (256, 16)))

@@ -149,6 +149,10 @@ def test_pack_unpack_roundtrip(fmt, n, k):
     if fmt == NVFP4:
         assert torch.equal(back.block_scales, wq.block_scales)
     assert torch.equal(back.tensor_scale, wq.tensor_scale)
-    # the packed image is a permutation: same multiset of code bytes
-    body = host(packed)[256:256 + host(wq.codes).size]
-    assert np.array_equal(np.sort(body), np.sort(host(wq.codes).reshape(-1)))
+    # the packed image is a permutation of the codes plus zero padding rows
+    # (panels of 32 rows)
+    codes = host(wq.codes)
+    pad_rows = (-n) % 32
+    body = host(packed)[256:256 + codes.size + pad_rows * codes.shape[1]]
+    expect = np.concatenate([codes.reshape(-1), np.zeros(pad_rows * codes.shape[1], np.uint8)])
+    assert np.array_equal(np.sort(body), np.sort(expect))

@@ -12,7 +12,7 @@ input shaped like the paper's workloads:
 Weights are quantized and packed once before timing (offline PTQ). Inputs
 are resident in HBM when the timed region starts.
 
-Prints ONE JSON line (the driver's contract) with the aggregate quantized
+Prints one JSON line with the aggregate quantized
 GEMM throughput of the step, a per-part breakdown, a roofline entry for the
 dominant kernel (per-launch HIP events on the launch stream) and the CPU
 oracle timed on a bounded sample.
@@ -55,8 +55,8 @@ def dev_bf16(bits):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path "
+              "(column/token sharding is a design note only); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -4,9 +4,11 @@
 // linears of the paper's denoising transformer (Sec. 4, quantization
 // paragraph; Table 2) and of its small text encoder (weight-only).
 //
-// One kernel template, three operand modes, all on 32x32 MFMAs:
+// Three operand modes, all on 32x32 MFMAs:
 //   W8A8  (FP8 x FP8)    : codes go straight into v_mfma_f32_32x32x64_f8f6f4
 //                          (OCP E4M3 operands); tensor scales in the epilogue.
+//                          Kernels of their own: k_gemm_fp8_direct for large
+//                          token counts, k_gemm_fp8 for small ones.
 //   W4A4  (NVFP4 x NVFP4): the E4M3 block scale changes every 16 reduction
 //                          elements and is not a power of two, so it cannot
 //                          ride in the hardware's per-32 power-of-two operand
@@ -19,20 +21,28 @@
 //                          (exact) for v_mfma_f32_32x32x16_bf16.
 //
 // Reduction order. Both operands of a 32x32 MFMA are read in the same
-// permuted reduction order: within a 128-wide chunk, lane l (row l % 32,
-// half g = l / 32) feeds the elements [64 g, 64 g + 64) of its row over the
-// chunk's MFMA steps, so each lane's operand bytes are one contiguous run
-// (the order of the sum changes, its terms do not).
+// permuted reduction order, so each lane's operand bytes are contiguous runs
+// (the order of the sum changes, its terms do not). Lane l covers row l % 32
+// and half g = l / 32:
+//   FP8  : in 64-wide step s of a 128-wide chunk, elements
+//          [64 s + 32 g, 64 s + 32 g + 32) of its row (one 2 KiB operand
+//          image per 32-row panel and step);
+//   NVFP4, W4A16: elements [64 g, 64 g + 64) of its row over the chunk's
+//          eight 16-wide steps.
 //
-// Tiling: a workgroup of WM x WN wavefronts owns a (32 TM WM) x (32 TN WN)
-// output tile; each wave owns TM x TN tiles of 32 x 32. Chunks of 128 are
-// staged in LDS in the packed weight's lane-major order, so every LDS read
-// is one contiguous 1 KiB wave access. Global loads run two chunks ahead in
-// two register sets; LDS is double buffered with one barrier per chunk.
+// Tiling of the shared NVFP4 / W4A16 template: a workgroup of WM x WN
+// wavefronts owns a (32 TM WM) x (32 TN WN) output tile; each wave owns
+// TM x TN tiles of 32 x 32. Chunks of 128 are staged in LDS in the packed
+// weight's lane-major order, so every LDS read is one contiguous 1 KiB wave
+// access. Global loads run one chunk ahead; LDS is double buffered with one
+// barrier per chunk.
 //
 // MFMA orientation: the weight panel is the MFMA A operand and the
 // activation panel the B operand, so a lane ends with runs of 4 consecutive
-// output columns of one output row (8-byte bf16 stores).
+// output columns of one output row.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -60,7 +70,6 @@ struct GemmArgs {
 // LDS bytes per 32-row panel per 128-chunk: codes/values of A (activations)
 // and B (weights), and expanded block scales of A and B.
 template <int MODE> struct Lds;
-template <> struct Lds<MODE_FP8> { static constexpr int A = 4096, B = 4096, AS = 0, BS = 0; };
 template <> struct Lds<MODE_NVFP4> { static constexpr int A = 2048, B = 2048, AS = 512, BS = 512; };
 template <> struct Lds<MODE_W4A16> { static constexpr int A = 8192, B = 2048, AS = 0, BS = 1024; };
 
@@ -125,6 +134,7 @@ __device__ inline void tile_coords(int id, int tiles_m, int tiles_n, int& bm, in
 
 template <int MODE, int WM, int WN, int TM, int TN, int DEPTH>
 __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
+  static_assert(MODE == MODE_NVFP4 || MODE == MODE_W4A16, "W8A8 has kernels of its own");
   constexpr int NT = 64 * WM * WN;
   constexpr int PA = TM * WM, PB = TN * WN;  // 32-row panels per tile
   constexpr int BM = 32 * PA, BN = 32 * PB;
@@ -136,7 +146,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   static_assert(NPA % NT == 0 && NPB % NT == 0, "piece count must divide the thread count");
   constexpr int RA = NPA / NT, RB = NPB / NT;
   constexpr int NSA = (MODE == MODE_NVFP4) ? BM : 0;
-  constexpr int NSB = (MODE == MODE_FP8) ? 0 : BN;
+  constexpr int NSB = BN;
   constexpr int RSA = (NSA + NT - 1) / NT, RSB = (NSB + NT - 1) / NT;
   constexpr int PIECES_A = Lds<MODE>::A / 16, PIECES_B = Lds<MODE>::B / 16;  // per panel chunk
 
@@ -154,7 +164,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   // each piece a thread copies is one 32-bit offset, the chunk advance is the
   // scalar offset, and rows or panels past the end fall outside the buffer's
   // range, which the hardware turns into zeros -- no branches, no clamping.
-  const int64_t a_row_bytes = (MODE == MODE_FP8) ? g.lda : (MODE == MODE_NVFP4) ? (int64_t)(g.k >> 1) : 2 * g.lda;
+  const int64_t a_row_bytes = (MODE == MODE_NVFP4) ? (int64_t)(g.k >> 1) : 2 * g.lda;
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * a_row_bytes), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
@@ -162,7 +172,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   const __amdgpu_buffer_rsrc_t rs_sa = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a_bscale), 0, (MODE == MODE_NVFP4) ? (int)((int64_t)g.m * (g.k >> 4)) : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_sb = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(g.w_scales), 0, (MODE == MODE_FP8) ? 0 : (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
 
   // Activation pieces are read row-contiguously (CPR 16-byte pieces cover a
   // row's chunk bytes, so 64 lanes read 64 / CPR whole row runs) and written
@@ -171,7 +181,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   // slot ((r + 32 g) ^ c) of LDS block h. The lanes of one row then hit
   // distinct LDS banks, and the operand read of lane l (slot l ^ (h + HALF g))
   // stays a conflict-free 1 KiB access.
-  constexpr int CPR = (MODE == MODE_FP8) ? 8 : (MODE == MODE_NVFP4) ? 4 : 16;
+  constexpr int CPR = (MODE == MODE_NVFP4) ? 4 : 16;
   constexpr int HALF = CPR / 2;
   uint32_t oa[RA];
   uint32_t la[RA];
@@ -216,7 +226,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
 
   // ---- global -> registers for chunk kc
   auto load_chunk = [&](Regs& R, int kc) {
-    const int sa_off = (MODE == MODE_FP8) ? kc * 128 : (MODE == MODE_NVFP4) ? kc * 64 : kc * 256;
+    const int sa_off = (MODE == MODE_NVFP4) ? kc * 64 : kc * 256;
 #pragma unroll
     for (int it = 0; it < RA; ++it) R.a[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[it], sa_off, 0);
 #pragma unroll
@@ -275,28 +285,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
     const uint8_t* ssa = st + A_BYTES + B_BYTES;
     const uint8_t* ssb = ssa + AS_BYTES;
     const int r = lane & 31, gq = lane >> 5;
-    if (MODE == MODE_FP8) {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        v8i fa[TM];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const uint8_t* p = sa + (wm * TM + i) * 4096 + s * 2048;
-          const v4i lo = *reinterpret_cast<const v4i*>(p + ((lane ^ (2 * s + 4 * gq)) * 16));
-          const v4i hi = *reinterpret_cast<const v4i*>(p + 1024 + ((lane ^ (2 * s + 1 + 4 * gq)) * 16));
-          fa[i] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const uint8_t* p = sb + (wn * TN + j) * 4096 + s * 2048 + lane * 16;
-          const v4i lo = *reinterpret_cast<const v4i*>(p), hi = *reinterpret_cast<const v4i*>(p + 1024);
-          const v8i fb = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb, fa[i], acc[i][j], 0, 0, 0, 0, 0, 0);
-        }
-      }
-    } else if (MODE == MODE_NVFP4) {
+    if (MODE == MODE_NVFP4) {
       uint2 sca[TM], scb[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) sca[i] = *reinterpret_cast<const uint2*>(ssa + (wm * TM + i) * 512 + r * 16 + 8 * gq);
@@ -432,6 +421,499 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   }
 }
 
+// Buffer descriptor of the activation codes: exactly the bytes a caller must
+// provide, (m - 1) * lda + k, so reads past the last row's k bytes are out of
+// range and return zeros. All offsets go in the per-lane offset, which is what
+// the hardware range-checks.
+__device__ __attribute__((always_inline)) inline __amdgpu_buffer_rsrc_t rsrc_a_fp8(const GemmArgs& g) {
+  const int64_t bytes = (g.m > 0) ? (int64_t)(g.m - 1) * g.lda + g.k : 0;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)bytes, 0x00020000);
+}
+
+// ---------------------------------------------------------------- FP8 (W8A8), few tokens
+// Four wavefronts (one per SIMD) on a (64 TM) x (64 TN) tile, each owning
+// TM x TN MFMA tiles of 32 x 32 (used with TM = 1, TN = 2: 64 x 128 tiles,
+// so that a short activation still spreads over many workgroups). The
+// reduction advances in steps of 64 --
+// one v_mfma_f32_32x32x64_f8f6f4 per tile and step -- through three LDS
+// stages, so that LDS traffic is spread evenly over every step instead of
+// bursting after a barrier:
+//   during step t: the MFMAs of step t run on fragments already in registers,
+//   interleaved with the LDS reads of step t+1's fragments (stage (t+1) % 3,
+//   written during step t-1), the LDS writes of step t+2 (registers loaded
+//   two steps ago) and the global loads of step t+4; one barrier per step.
+// A stage is rewritten two steps after it was last read, so one barrier per
+// step separates every write from the reads before and after it. The loop
+// body has no branches: loads past the last step get an out-of-range offset
+// and read zeros, and LDS traffic past the end lands in stages nobody reads
+// again. The packed weight keeps each 64-wide step of a 32-row
+// panel as one contiguous 2 KiB operand image; activation rows are read
+// row-contiguously and stored through the XOR swizzle of k_gemm.
+template <int TM, int TN>
+__global__ void __launch_bounds__(256) k_gemm_fp8(GemmArgs g) {
+  constexpr int NT = 256;
+  constexpr int PA = 2 * TM, PB = 2 * TN;                 // 32-row panels per tile
+  constexpr int BM = 32 * PA, BN = 32 * PB;
+  constexpr int A_BYTES = PA * 2048, B_BYTES = PB * 2048, STAGE = A_BYTES + B_BYTES;
+  constexpr int NPA = A_BYTES / 16, NPB = B_BYTES / 16;   // 16-byte pieces per step
+  static_assert(NPA % NT == 0 && NPB % NT == 0, "every thread copies whole pieces: no guards in the loop");
+  constexpr int RA = NPA / NT, RB = NPB / NT;
+  constexpr int NS = 3;                                   // LDS stages
+  __shared__ __attribute__((aligned(16))) uint8_t smem[NS * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int gq = lane >> 5;
+  int bm, bn;
+  tile_coords(blockIdx.x, g.tiles_m, g.tiles_n, bm, bn);
+  const int m0 = bm * BM, n0 = bn * BN;
+  const int steps = g.k >> 6;
+  const int npanels_w = (g.n + 31) >> 5;
+  const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * steps * 2048), 0x00020000);
+
+  // activation piece c (0..3) of row rr: bytes [16 c, 16 c + 16) of the step,
+  // lane half g = c / 2, piece h = c % 2, swizzled slot (rr + 32 g) ^ c
+  uint32_t oa[RA], la[RA], ob[RB], lb[RB];
+#pragma unroll
+  for (int it = 0; it < RA; ++it) {
+    const int q = it * NT + tid;
+    const int p = q >> 7, rr = (q >> 2) & 31, c = q & 3;
+    const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
+    oa[it] = (row < (uint32_t)g.m) ? row * (uint32_t)g.lda + 16u * c : 0x80000000u;
+    la[it] = (uint32_t)(p * 2048 + (c & 1) * 1024 + (((rr + 32 * (c >> 1)) ^ c) * 16));
+  }
+#pragma unroll
+  for (int it = 0; it < RB; ++it) {
+    const int q = it * NT + tid;
+    const uint32_t panel = (uint32_t)((n0 >> 5) + (q >> 7));
+    ob[it] = (panel < (uint32_t)npanels_w) ? panel * (uint32_t)(steps * 2048) + 16u * (q & 127) : 0x80000000u;
+    lb[it] = (uint32_t)(A_BYTES + 16 * q);
+  }
+
+  v4i ra[2][RA], rb[2][RB];
+  // offsets of steps past the last one get the top bit: out of range for any base
+  auto gload = [&](int set, int t) __attribute__((always_inline)) {
+    const uint32_t hi = t < steps ? 0u : 0x80000000u;
+#pragma unroll
+    for (int it = 0; it < RA; ++it) ra[set][it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[it] + t * 64) | hi, 0, 0);
+#pragma unroll
+    for (int it = 0; it < RB; ++it) rb[set][it] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, (ob[it] + t * 2048) | hi, 0, 0);
+  };
+  auto lds_write = [&](int set, uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) *reinterpret_cast<v4i*>(st + la[it]) = ra[set][it];
+#pragma unroll
+    for (int it = 0; it < RB; ++it) *reinterpret_cast<v4i*>(st + lb[it]) = rb[set][it];
+  };
+  v8i fa[2][TM], fb[2][TN];
+  auto frag_read = [&](int set, const uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const uint8_t* p = st + (wm * TM + i) * 2048;
+      const v4i lo = *reinterpret_cast<const v4i*>(p + ((lane ^ (2 * gq)) * 16));
+      const v4i hi = *reinterpret_cast<const v4i*>(p + 1024 + ((lane ^ (1 + 2 * gq)) * 16));
+      fa[set][i] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const uint8_t* p = st + A_BYTES + (wn * TN + j) * 2048 + lane * 16;
+      const v4i lo = *reinterpret_cast<const v4i*>(p), hi = *reinterpret_cast<const v4i*>(p + 1024);
+      fb[set][j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    }
+  };
+  v16f acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+  constexpr int NMF = TM * TN, NRD = 2 * (TM + TN), NWR = RA + RB, NLD = RA + RB;
+  auto step_body = [&](int set, int t) __attribute__((always_inline)) {
+    // t = current step; fragments of t are in fa/fb[set]
+    uint8_t* rd = smem + ((t + 1) % NS) * STAGE;
+    uint8_t* wr = smem + ((t + 2) % NS) * STAGE;
+    frag_read(set ^ 1, rd);
+    lds_write(set, wr);   // set == t % 2: the register set holding step t + 2
+    gload(set, t + 4);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0, 0, 0, 0);
+    // interleave: each MFMA followed by its share of LDS reads, writes and loads
+#pragma unroll
+    for (int t2 = 0; t2 < NMF; ++t2) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (t2 < NRD) __builtin_amdgcn_sched_group_barrier(0x100, (NRD + NMF - 1) / NMF, 0);
+      if (t2 < NWR) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      if (t2 < NLD) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  if (steps > 0) {
+    // prologue: stages 0 and 1 filled, registers hold steps 2 and 3
+    gload(0, 0);
+    gload(1, 1);
+    lds_write(0, smem);
+    lds_write(1, smem + STAGE);
+    __syncthreads();
+    gload(0, 2);
+    gload(1, 3);
+    frag_read(0, smem);
+    // steps = k / 64 is even (k % 128 == 0): two steps per iteration, one per register set
+    for (int t = 0; t < steps; t += 2) {
+      step_body(0, t);
+      step_body(1, t + 1);
+    }
+  }
+
+  const float c = *g.w_tscale * *g.a_tscale;
+  const bool vec = ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 3) == 0);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + (wm * TM + i) * 32 + (lane & 31);
+    if (m >= g.m) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int n = n0 + (wn * TN + j) * 32 + 8 * qd + 4 * gq;
+        if (n >= g.n) continue;
+        const float v0 = acc[i][j][4 * qd] * c, v1 = acc[i][j][4 * qd + 1] * c;
+        const float v2 = acc[i][j][4 * qd + 2] * c, v3 = acc[i][j][4 * qd + 3] * c;
+        if (g.f32out) {
+          float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+          if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
+          else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
+        } else {
+          uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+          const uint32_t w0 = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
+          const uint32_t w1 = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
+          if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
+          else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
+        }
+      }
+    }
+  }
+}
+
+template <int TM, int TN>
+static hipError_t run_fp8(GemmArgs g, hipStream_t st) {
+  g.tiles_m = (g.m + 64 * TM - 1) / (64 * TM);
+  g.tiles_n = (g.n + 64 * TN - 1) / (64 * TN);
+  hipLaunchKernelGGL((k_gemm_fp8<TM, TN>), dim3(g.tiles_m * g.tiles_n), dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- FP8, 256 x 256 tiles
+// Two fp32 values to a pair of bf16 (low half = a), round to nearest even
+// (one v_cvt_pk_bf16_f32).
+__device__ __attribute__((always_inline)) inline uint32_t pk_bf16(float a, float b) {
+  typedef float v2f_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 v2bf_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f_t){a, b}, v2bf_t));
+}
+
+// Epilogue shared by the FP8 kernels: a wave's TM x TN accumulator tiles,
+// first output row mw and column nw, scaled by c and rounded to the output
+// type. Lane l holds Y[mw + 32 i + l % 32][nw + 32 j + 8 q + 4 (l / 32) + e].
+template <int TM, int TN>
+__device__ __attribute__((always_inline)) inline void store_tiles(const GemmArgs& g, const v16f (&acc)[TM][TN],
+                                                                  int mw, int nw, int lane, float c) {
+  const bool vec = ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 3) == 0);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = mw + 32 * i + (lane & 31);
+    if (m >= g.m) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int n = nw + 32 * j + 8 * qd + 4 * (lane >> 5);
+        if (n >= g.n) continue;
+        const float v0 = acc[i][j][4 * qd] * c, v1 = acc[i][j][4 * qd + 1] * c;
+        const float v2 = acc[i][j][4 * qd + 2] * c, v3 = acc[i][j][4 * qd + 3] * c;
+        if (g.f32out) {
+          float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+          if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
+          else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
+        } else {
+          uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+          const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
+          if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
+          else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
+        }
+      }
+    }
+  }
+}
+
+// Epilogue fast path: bf16 output, whole tile inside the output, 16-byte
+// aligned rows. Stored straight from the MFMA layout, every store
+// instruction would scatter 8-byte pieces over 32 rows, which the memory
+// pipeline takes one cache line at a time; here each 32-row block of the
+// wave's tile is converted into the wave's private LDS area in the MFMA
+// layout (row pitch padded by 16 bytes so the 32 rows spread over all
+// banks) and read back 16 bytes per lane in row order, so that every store
+// instruction writes four whole 256-byte row segments. Each wave reads back
+// only what it wrote, so no barrier is needed; all addresses are one base
+// register plus immediate offsets. `stage` holds 32 * (64 TN + 16) bytes.
+template <int TM, int TN>
+__device__ __attribute__((always_inline)) inline void store_tiles_fast(const GemmArgs& g, const v16f (&acc)[TM][TN],
+                                                                       uint8_t* stage, int mw, int nw, int lane,
+                                                                       float c) {
+  constexpr int RB = 64 * TN, PITCH = RB + 16, PPR = RB / 16, ROWS_PER_IT = 64 / PPR;
+  static_assert(64 % PPR == 0, "a wave reads whole rows per instruction");
+  uint8_t* wr = stage + (lane & 31) * PITCH + 8 * (lane >> 5);
+  const uint8_t* rd = stage + (lane / PPR) * PITCH + 16 * (lane % PPR);
+  uint8_t* out = reinterpret_cast<uint8_t*>(g.y) + ((int64_t)(mw + lane / PPR) * g.ldy + nw + 8 * (lane % PPR)) * 2;
+  const int64_t it_stride = (int64_t)ROWS_PER_IT * g.ldy * 2;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd)
+        *reinterpret_cast<uint2*>(wr + (32 * j + 8 * qd) * 2) =
+            make_uint2(pk_bf16(acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c),
+                       pk_bf16(acc[i][j][4 * qd + 2] * c, acc[i][j][4 * qd + 3] * c));
+    uint8_t* o = out + (int64_t)i * 32 * 2 * g.ldy;
+#pragma unroll
+    for (int it = 0; it < 32 / ROWS_PER_IT; ++it)
+      *reinterpret_cast<uint4*>(o + it * it_stride) = *reinterpret_cast<const uint4*>(rd + it * ROWS_PER_IT * PITCH);
+  }
+}
+
+// Activation staging shared by the 256 x 256 FP8 kernels: 256 rows x one
+// 128-byte chunk, read row-contiguously (8 lanes per row) and stored in LDS
+// as 8 panels of 4 KiB. Piece c (bytes 16c .. 16c+15 of the row's chunk)
+// belongs to step s = c / 4, lane half g = (c / 2) % 2 and register half
+// h = c % 2 of the MFMA operand, so it lands in 1 KiB block 2s + h of its
+// panel at slot (r + 32 g) ^ c: the eight lanes of a row spread over banks,
+// and the operand read of lane l (slot l ^ (4s + 2g + h)) is a permutation of
+// one contiguous 1 KiB block -- conflict free.
+struct AStage256 {
+  static constexpr int RA = 8;  // pieces per thread per chunk
+  uint32_t oa[RA], la[RA];
+  __device__ __attribute__((always_inline)) inline void init(const GemmArgs& g, int m0, int tid) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) {
+      const int q = it * 256 + tid;
+      const int p = q >> 8, rr = (q >> 3) & 31, c = q & 7;
+      const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
+      oa[it] = (row < (uint32_t)g.m) ? row * (uint32_t)g.lda + 16u * c : 0x80000000u;
+      la[it] = (uint32_t)(p * 4096 + (2 * (c >> 2) + (c & 1)) * 1024 + (((rr + 32 * ((c >> 1) & 1)) ^ c) * 16));
+    }
+  }
+};
+
+// Operand fragment of activation panel `panel`, step s (0/1) of a staged chunk.
+__device__ __attribute__((always_inline)) inline v8i read_a_frag(const uint8_t* st, int panel, int s, int lane) {
+  const int x = 4 * s + 2 * (lane >> 5);
+  const uint8_t* p = st + panel * 4096 + s * 2048;
+  const v4i lo = *reinterpret_cast<const v4i*>(p + ((lane ^ x) * 16));
+  const v4i hi = *reinterpret_cast<const v4i*>(p + 1024 + ((lane ^ (x + 1)) * 16));
+  return (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+}
+
+// W8A8, weights straight from memory. Same tile and wave layout, but each
+// wave loads its weight fragments from the packed buffer directly into
+// registers -- the packed layout is already the operand image, one
+// contiguous 1 KiB per wave load -- one chunk ahead, in two register sets.
+// Only the activations pass through LDS, which halves LDS traffic (32 KiB of
+// writes and 64 KiB of reads per chunk instead of 64 and 128) at the price
+// of each weight chunk being fetched by the two waves that share it (the
+// second fetch normally hits the CU's L1). Activation fragments are read
+// just in time, one 32-row panel ahead of the MFMAs that use it.
+//
+// The grid is persistent (at most one workgroup per CU, each walking the
+// tiles blockIdx.x, + gridDim.x, ...), so a workgroup's next tile starts
+// loading while the stores of its previous tile drain. Prefetches that would
+// run past the last chunk of a tile are turned into out-of-range loads,
+// which return zeros without touching memory.
+__global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
+  constexpr int A_STAGE = 8 * 4096;
+  constexpr int RA = AStage256::RA;
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int OUT_STAGE = 32 * (64 * 4 + 16);  // per wave: 32 rows of 128 bf16 + pad
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t sout[4 * OUT_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const float scale = *g.w_tscale * *g.a_tscale;
+  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 4096), 0x00020000);
+
+  AStage256 A;
+  uint32_t ob[4];
+  v4i ga[RA];
+  v8i fb[2][2][4];  // [chunk parity][step][weight panel]
+  v8i fa[2];
+  v16f acc[4][4];
+
+  // Offsets of chunks past the last one get the top bit set: out of range
+  // for every valid or invalid base (a uniform OR, no branch in the loop).
+  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  auto load_a = [&](int kc) __attribute__((always_inline)) {
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int it = 0; it < RA; ++it)
+      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + kc * 128) | hi, 0, 0);
+  };
+  auto write_a = [&](uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) *reinterpret_cast<v4i*>(st + A.la[it]) = ga[it];
+  };
+  // weight fragments of chunk kc into set P: (step, panel) in load order
+  auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t o = (ob[j] + kc * 4096 + s * 2048) | hi;
+        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
+        const v4i hi = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
+        fb[P][s][j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      }
+  };
+  // MFMA group f = (step f / 4, activation panel f % 4) on fragment fa[f % 2]
+  auto mgroup = [&](auto Pc, int f) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[f & 3][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[P][f >> 2][j], fa[f & 1], acc[f & 3][j], 0, 0, 0, 0, 0, 0);
+  };
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    // step 0: weight loads of chunk kc + 1, activation fragments 1..4
+    load_b(std::integral_constant<int, P ^ 1>(), kc + 1);
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      fa[(f + 1) & 1] = read_a_frag(cur, wm * 4 + ((f + 1) & 3), (f + 1) >> 2, lane);
+      mgroup(Pc, f);
+    }
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (weights)
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // step 1, groups 4..6: stage activations of chunk kc + 1, load kc + 2.
+    // The LDS writes sit between the fragment reads in program order (the
+    // compiler cannot tell the two stages apart, so it keeps LDS accesses in
+    // that order); each activation load follows the write of its register.
+    const uint32_t a_hi = past(kc + 2);
+#pragma unroll
+    for (int f = 4; f < 7; ++f) {
+      fa[(f + 1) & 1] = read_a_frag(cur, wm * 4 + ((f + 1) & 3), (f + 1) >> 2, lane);
+#pragma unroll
+      for (int it = 3 * (f - 4); it < 3 * (f - 3) && it < RA; ++it)
+        *reinterpret_cast<v4i*>(nxt + A.la[it]) = ga[it];
+      mgroup(Pc, f);
+#pragma unroll
+      for (int it = 3 * (f - 4); it < 3 * (f - 3) && it < RA; ++it)
+        ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + (kc + 2) * 128) | a_hi, 0, 0);
+    }
+#pragma unroll
+    for (int f = 4; f < 7; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (t < 3 && 3 * (f - 4) + t < RA) {
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (activations)
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // group 7 covers the read of the next chunk's first fragment
+    fa[0] = read_a_frag(nxt, wm * 4, 0, lane);
+    mgroup(Pc, 7);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 256, n0 = bn * 256;
+    A.init(g, m0, tid);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 4 + j);
+      ob[j] = (panel < (uint32_t)npanels_w) ? panel * (uint32_t)(kcn * 4096) + 16u * lane : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    // An odd chunk count takes its first chunk unpipelined, so that the
+    // pipelined loop always runs whole pairs of chunks (register set 0, then
+    // 1) and nothing follows it.
+    int kc = 0;
+    if (kcn & 1) {
+      load_a(0);
+      write_a(smem);
+      load_b(std::integral_constant<int, 0>(), 0);
+      __syncthreads();
+#pragma unroll
+      for (int f = 0; f < 8; ++f) {
+        fa[f & 1] = read_a_frag(smem, wm * 4 + (f & 3), f >> 2, lane);
+        mgroup(std::integral_constant<int, 0>(), f);
+      }
+      __syncthreads();
+      kc = 1;
+    }
+    if (kc < kcn) {
+      load_a(kc);
+      write_a(smem);
+      __syncthreads();
+      load_a(kc + 1);
+      load_b(std::integral_constant<int, 0>(), kc);
+      fa[0] = read_a_frag(smem, wm * 4, 0, lane);
+      for (; kc < kcn; kc += 2) {
+        chunk(std::integral_constant<int, 0>(), kc);
+        chunk(std::integral_constant<int, 1>(), kc + 1);
+      }
+    }
+    // Every operand write of this tile happened before its last barrier; the
+    // next tile's first write to stage 0 can only race with the discarded
+    // fragment read after that barrier.
+    if (fast_out && m0 + 256 <= g.m && n0 + 256 <= g.n)
+      store_tiles_fast<4, 4>(g, acc, sout + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, scale);
+    else
+      store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, scale);
+  }
+}
+
 // ---------------------------------------------------------------- W4A16, few tokens
 // bf16 activations with at most 32 * MT rows against NVFP4 weights: the
 // weight stream is the whole cost, so one workgroup owns one 32-row weight
@@ -515,6 +997,20 @@ static hipError_t run(GemmArgs g, hipStream_t st) {
 
 
 
+// Compute units of the current device, queried once per device. Persistent
+// grids launch at most this many workgroups.
+static int device_cus() {
+  static int cache[64];  // 0 = not queried yet
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    __atomic_store_n(&cache[dev], n, __ATOMIC_RELAXED);
+  }
+  return n;
+}
+
 hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const float* a_tscale,
                        int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
                        void* y, int64_t ldy, bool f32out, hipStream_t st) {
@@ -542,8 +1038,12 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   // Large tiles: 256 x 256 per workgroup, 8 wavefronts (two per SIMD, so
   // one wave's MFMAs cover the other's LDS and barrier waits), 128 x 64 each.
   if (a_fmt == 1) {
-    if (m <= 128) return run<MODE_FP8, 2, 2, 1, 2>(g, st);
-    return run<MODE_FP8, 2, 4, 4, 2>(g, st);
+    if (m <= 128) return run_fp8<1, 2>(g, st);
+    g.tiles_m = (g.m + 255) / 256;
+    g.tiles_n = (g.n + 255) / 256;
+    const int tiles = g.tiles_m * g.tiles_n;
+    hipLaunchKernelGGL(k_gemm_fp8_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    return hipGetLastError();
   } else if (a_fmt == 2) {
     if (m <= 128) return run<MODE_NVFP4, 2, 2, 1, 2>(g, st);
     return run<MODE_NVFP4, 2, 4, 4, 2>(g, st);

@@ -17,7 +17,7 @@ namespace qg {
 // The weight is stored in panels of 32 rows (n rounded up to a multiple of
 // 32, padding rows are zero codes) and chunks of 128 reduction elements.
 constexpr uint32_t kPackMagic = 0x57504751u;  // "QGPW"
-constexpr uint32_t kPackVersion = 2u;
+constexpr uint32_t kPackVersion = 3u;
 constexpr int64_t kPackHeader = 256;
 constexpr int64_t kPackScaleOffset = 32;
 constexpr int64_t kPanel = 32;

@@ -9,7 +9,9 @@
 // 32x32 MFMAs once the reduction index is permuted the same way for both
 // operands. A lane's bytes are split into 16-byte pieces h, stored as
 // [h][lane][16 B], so that each piece is one contiguous 1 KiB wave access:
-//   FP8  : 4096-byte chunk, piece h of lane l = row r, bytes 64 g + 16 h;
+//   FP8  : 4096-byte chunk made of two 2048-byte steps of 64 reduction
+//          elements; in step t, piece h of lane l = row r, bytes
+//          64 t + 32 g + 16 h (each step is one self-contained MFMA operand);
 //   NVFP4: 2048-byte code chunk, piece h of lane l = row r, bytes 32 g + 16 h;
 //          block scales in their own region, 256 bytes per chunk = [row][8].
 // Chunks of one panel follow each other along k, so a panel is one
@@ -44,7 +46,7 @@ __device__ inline int64_t canon_piece(int fmt, int64_t p, int64_t n, int64_t k) 
   const int64_t h = s >> 6, l = s & 63;
   const int64_t row = panel * 32 + (l & 31);
   if (row >= n) return -1;
-  if (fmt == 1) return row * k + kc * 128 + 64 * (l >> 5) + 16 * h;
+  if (fmt == 1) return row * k + kc * 128 + 64 * (h >> 1) + 32 * (l >> 5) + 16 * (h & 1);
   return row * (k / 2) + kc * 64 + 32 * (l >> 5) + 16 * h;
 }
 

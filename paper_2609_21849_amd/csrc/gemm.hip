@@ -914,6 +914,270 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------------- W4A4 (NVFP4), large token counts
+// Four E4M3 block scales (one dword, block b in byte b; never negative) to
+// fp16, exact: the E4M3 bit pattern shifted into the fp16 field is the value
+// divided by 2^8 (normal and subnormal alike), and the multiply by 2^8 lands
+// in the fp16 normal range. Result: .x = blocks 0 and 1, .y = blocks 2 and 3.
+__device__ __attribute__((always_inline)) inline uint2 e4m3x4_to_f16x4(uint32_t d) {
+  const v2h k256 = {(_Float16)256.0f, (_Float16)256.0f};
+  const uint32_t lo = ((d & 0x7Fu) << 7) | ((d & 0x7F00u) << 15);
+  const uint32_t hi = ((d & 0x7F0000u) >> 9) | ((d & 0x7F000000u) >> 1);
+  return make_uint2(__builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, lo) * k256),
+                    __builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, hi) * k256));
+}
+
+// fp16 block scale b (0..3) of a lane's four.
+__device__ __attribute__((always_inline)) inline _Float16 scale_f16(uint2 sc, int b) {
+  const uint32_t w = (b < 2) ? sc.x : sc.y;
+  return __builtin_bit_cast(_Float16, (uint16_t)((b & 1) ? (w >> 16) : (w & 0xFFFFu)));
+}
+
+// W4A4 on 256 x 256 tiles, four wavefronts (one per SIMD) of 128 x 128 =
+// 4 x 4 MFMA tiles of 32 x 32 -- the largest wave tile, which minimises the
+// operand expansion per MFMA: each lane expands 8 fragments of 8 elements per
+// 16-wide step for 16 MFMAs. Per 128-wide chunk: 128 v_mfma_f32_32x32x16_f16
+// (4096 MFMA cycles) against ~600 VALU operations of expansion.
+//   weights     : codes (2 x 1 KiB wave loads per panel) and E4M3 block scales
+//                 (one dword per lane) straight from the packed buffer into
+//                 registers, one chunk ahead, two register sets;
+//   activations : codes and block scales staged in LDS per chunk (scales
+//                 converted to fp16 once per workgroup while staging);
+//   expansion   : software-pipelined one step ahead of the MFMAs that use it,
+//                 into two sets of fp16 fragments.
+// One barrier per chunk, after step 6; step 7 reads the next chunk's first
+// activation fragments. Persistent grid and staged epilogue as in
+// k_gemm_fp8_direct.
+__global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
+  constexpr int A_CODES = 8 * 2048;              // 256 rows x 64 B of codes
+  constexpr int A_STAGE = A_CODES + 256 * 16;    // + 256 rows x 8 fp16 scales
+  constexpr int OUT_STAGE = 32 * (64 * 4 + 16);
+  constexpr uint32_t OOB = 0x80000000u;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t sout[4 * OUT_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 31, gq = lane >> 5;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const float scale = *g.w_tscale * *g.a_tscale;
+  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const uint32_t ka = (uint32_t)(g.k >> 1), ks = (uint32_t)(g.k >> 4);  // A code / scale bytes per row
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * ka), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a_bscale), 0, (int)((int64_t)g.m * ks), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 2048), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_bs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
+
+  uint32_t oa[4], la[4], osa, ob[4], osb[4];
+  v4i ga[4];        // staged activation codes of a chunk
+  v2i gs;           // staged activation scales (one row per thread)
+  v4i bc[2][4][2];  // weight codes [chunk parity][panel][half]
+  uint32_t bs[2][4];  // weight E4M3 scales [chunk parity][panel]
+  uint2 bf[4];      // weight fp16 scales of the current chunk
+  v4i ac[2][4];     // activation codes [half][panel] of the current chunk
+  uint2 af[4];      // activation fp16 scales of the current chunk
+  v8h fa[2][4], fb[2][4];  // expanded fragments, two steps
+  v16f acc[4][4];
+
+  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  auto load_a = [&](int kc) __attribute__((always_inline)) {
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int it = 0; it < 4; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[it] + kc * 64) | hi, 0, 0);
+    gs = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + kc * 8) | hi, 0, 0);
+  };
+  auto write_a_codes = [&](uint8_t* st, int from, int to) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+      if (it >= from && it < to) *reinterpret_cast<v4i*>(st + la[it]) = ga[it];
+  };
+  auto write_a_scales = [&](uint8_t* st) __attribute__((always_inline)) {
+    const uint2 lo = e4m3x4_to_f16x4((uint32_t)gs.x), hi = e4m3x4_to_f16x4((uint32_t)gs.y);
+    *reinterpret_cast<uint4*>(st + A_CODES + tid * 16) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+  auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t o = (ob[j] + kc * 2048) | hi;
+      bc[P][j][0] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
+      bc[P][j][1] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
+      bs[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + kc * 256) | hi, 0, 0);
+    }
+  };
+  auto read_a_half = [&](const uint8_t* st, int h) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      ac[h][i] = *reinterpret_cast<const v4i*>(st + (wm * 4 + i) * 2048 + h * 1024 + ((lane ^ (h + 2 * gq)) * 16));
+  };
+  auto read_a_scales = [&](const uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const uint2*>(st + A_CODES + ((wm * 4 + i) * 32 + r) * 16 + 8 * gq);
+  };
+  auto convert_b_scales = [&](auto Pc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bf[j] = e4m3x4_to_f16x4(bs[P][j]);
+  };
+  // expand step s (0..7) of the chunk held in ac / af and bc[P] / bf into set D
+  auto expand = [&](auto Pc, int s, int D) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const v4i c = ac[s >> 2][i];
+      const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
+      fa[D][i] = dequant8_f16(w, scale_f16(af[i], s >> 1));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const v4i c = bc[P][j][s >> 2];
+      const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
+      fb[D][j] = dequant8_f16(w, scale_f16(bf[j], s >> 1));
+    }
+  };
+  auto mfmas = [&](int D) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[D][j], fa[D][i], acc[i][j], 0, 0, 0);
+  };
+  // 16 MFMAs, each followed by its share of the expansion (64 VALU + scale work)
+  auto interleave = [&](int nvmem, int nds_r, int nds_w) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
+      if (t < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if (t < nds_r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (t < nds_w) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    }
+  };
+
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    constexpr std::integral_constant<int, P ^ 1> Q{};
+    // steps 0..3: weight loads of chunk kc + 1 (12 per lane), second code half
+    // of the activations read during step 2
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s == 0) load_b(Q, kc + 1);
+      if (s == 2) read_a_half(cur, 1);
+      mfmas(s & 1);
+      expand(Pc, s + 1, (s + 1) & 1);
+      interleave(s == 0 ? 12 : 0, s == 2 ? 4 : 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // steps 4, 5: stage the activations of chunk kc + 1, then load kc + 2
+#pragma unroll
+    for (int s = 4; s < 6; ++s) {
+      if (s == 4) write_a_codes(nxt, 0, 2);
+      else { write_a_codes(nxt, 2, 4); write_a_scales(nxt); }
+      if (s == 5) load_a(kc + 2);
+      mfmas(s & 1);
+      expand(Pc, s + 1, (s + 1) & 1);
+      interleave(s == 5 ? 5 : 0, 0, s == 4 ? 2 : 3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // step 6, then the barrier that publishes chunk kc + 1
+    mfmas(0);
+    expand(Pc, 7, 1);
+    interleave(0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // step 7 covers the next chunk's first reads and its step-0 expansion
+    read_a_half(nxt, 0);
+    read_a_scales(nxt);
+    convert_b_scales(Q);
+    mfmas(1);
+    expand(Q, 0, 0);
+    interleave(0, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 256, n0 = bn * 256;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int q = it * 256 + tid;
+      const int p = q >> 7, rr = (q >> 2) & 31, c = q & 3;
+      const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
+      oa[it] = (row < (uint32_t)g.m) ? row * ka + 16u * c : OOB;
+      la[it] = (uint32_t)(p * 2048 + (c & 1) * 1024 + (((rr + 32 * (c >> 1)) ^ c) * 16));
+    }
+    {
+      const uint32_t row = (uint32_t)(m0 + tid);
+      osa = (row < (uint32_t)g.m) ? row * ks : OOB;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 4 + j);
+      const bool in = panel < (uint32_t)npanels_w;
+      ob[j] = in ? panel * (uint32_t)(kcn * 2048) + 16u * lane : OOB;
+      osb[j] = in ? panel * (uint32_t)(kcn * 256) + 8u * r + 4u * gq : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    // An odd chunk count takes its first chunk unpipelined (see the W8A8 kernel).
+    int kc = 0;
+    if (kcn & 1) {
+      load_a(0);
+      load_b(std::integral_constant<int, 0>(), 0);
+      write_a_codes(smem, 0, 4);
+      write_a_scales(smem);
+      __syncthreads();
+      read_a_half(smem, 0);
+      read_a_half(smem, 1);
+      read_a_scales(smem);
+      convert_b_scales(std::integral_constant<int, 0>());
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        expand(std::integral_constant<int, 0>(), s, 0);
+        mfmas(0);
+      }
+      __syncthreads();
+      kc = 1;
+    }
+    if (kc < kcn) {
+      load_a(kc);
+      load_b(std::integral_constant<int, 0>(), kc);
+      write_a_codes(smem, 0, 4);
+      write_a_scales(smem);
+      __syncthreads();
+      load_a(kc + 1);
+      read_a_half(smem, 0);
+      read_a_scales(smem);
+      convert_b_scales(std::integral_constant<int, 0>());
+      expand(std::integral_constant<int, 0>(), 0, 0);
+      for (; kc < kcn; kc += 2) {
+        chunk(std::integral_constant<int, 0>(), kc);
+        chunk(std::integral_constant<int, 1>(), kc + 1);
+      }
+    }
+    if (fast_out && m0 + 256 <= g.m && n0 + 256 <= g.n)
+      store_tiles_fast<4, 4>(g, acc, sout + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, scale);
+    else
+      store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, scale);
+  }
+}
+
 // ---------------------------------------------------------------- W4A16, few tokens
 // bf16 activations with at most 32 * MT rows against NVFP4 weights: the
 // weight stream is the whole cost, so one workgroup owns one 32-row weight
@@ -1046,7 +1310,11 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     return hipGetLastError();
   } else if (a_fmt == 2) {
     if (m <= 128) return run<MODE_NVFP4, 2, 2, 1, 2>(g, st);
-    return run<MODE_NVFP4, 2, 4, 4, 2>(g, st);
+    g.tiles_m = (g.m + 255) / 256;
+    g.tiles_n = (g.n + 255) / 256;
+    const int tiles = g.tiles_m * g.tiles_n;
+    hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    return hipGetLastError();
   } else {
     if (m <= 64) {
       const unsigned grid = (unsigned)((n + 31) / 32);

@@ -84,21 +84,28 @@ __device__ inline v8h dequant8_f16(uint32_t w, _Float16 sc) {
 }
 
 // 8 E2M1 codes times an fp32 block scale -> 8 bf16 (exact, so the top half
-// of the fp32 product is already the bf16 value).
+// of the fp32 product is already the bf16 value): one conversion, two
+// multiplies and one byte permute per pair.
 __device__ inline v4i dequant8_bf16(uint32_t w, float sc) {
+  const auto t0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 0);
+  const auto t1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 1);
+  const auto t2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 2);
+  const auto t3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 3);
   v4i o;
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    float f0, f1;
-    switch (b) {
-      case 0: { auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 0); f0 = t[0]; f1 = t[1]; break; }
-      case 1: { auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 1); f0 = t[0]; f1 = t[1]; break; }
-      case 2: { auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 2); f0 = t[0]; f1 = t[1]; break; }
-      default: { auto t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 3); f0 = t[0]; f1 = t[1]; break; }
-    }
-    o[b] = (int)((f2u(f0 * sc) >> 16) | (f2u(f1 * sc) & 0xFFFF0000u));
-  }
+  o[0] = (int)__builtin_amdgcn_perm(f2u(t0[1] * sc), f2u(t0[0] * sc), 0x07060302u);
+  o[1] = (int)__builtin_amdgcn_perm(f2u(t1[1] * sc), f2u(t1[0] * sc), 0x07060302u);
+  o[2] = (int)__builtin_amdgcn_perm(f2u(t2[1] * sc), f2u(t2[0] * sc), 0x07060302u);
+  o[3] = (int)__builtin_amdgcn_perm(f2u(t3[1] * sc), f2u(t3[0] * sc), 0x07060302u);
   return o;
+}
+
+// Value of a non-negative E4M3 block-scale code (never NaN: the quantizer
+// saturates at 448), exactly: its 7 bits placed at the top of the fp32
+// mantissa/exponent field are the value times 2^-120 -- normal codes become
+// normal fp32 numbers, subnormal codes denormal ones -- and one multiply by
+// 2^120 restores it.
+__device__ inline float dec_e4m3_scale(uint32_t c) {
+  return u2f((c & 0x7Fu) << 20) * 1.329227995784915872903807060280344576e36f;  // 2^120
 }
 
 // 8 E4M3 block scales (two dwords, block j in byte j) -> 8 fp16 (exact).
@@ -1178,67 +1185,281 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   }
 }
 
-// ---------------------------------------------------------------- W4A16, few tokens
-// bf16 activations with at most 32 * MT rows against NVFP4 weights: the
-// weight stream is the whole cost, so one workgroup owns one 32-row weight
-// panel (32 output columns) and its NW wavefronts split the reduction
-// dimension chunk by chunk, reading the packed weight straight from HBM in
-// operand order (32 B of codes + 4 B of scales per lane per chunk, no LDS
-// staging). Partial accumulators are summed through LDS at the end.
-template <int MT, int NW>
-__global__ void __launch_bounds__(64 * NW) k_w4a16_skinny(GemmArgs g) {
+// ---------------------------------------------------------------- W4A16, up to 1024 tokens
+// bf16 activations against NVFP4 weights when the output is too small to
+// fill the chip with large tiles (the text-encoder linears). A workgroup
+// owns NP 32-row weight panels (32 NP output columns) and one block of 32 MT
+// activation rows; its NW wavefronts split the reduction dimension (chunk kc
+// goes to wave kc % NW) and their partial accumulators are summed through
+// LDS at the end, so a workgroup's latency is a few chunks, not K / 128 of
+// them. Every workgroup re-reads its activation rows, so NP sets how often
+// the activations cross L2 (M K 2 bytes per 32 NP output columns). Each wave
+// reads the packed weight straight from memory in operand order (32 B of
+// codes + 4 B of scales per lane, panel and chunk). Activations are
+// read row-contiguously (16 lanes per 256-byte row run of a chunk: 8 cache
+// lines per load instruction instead of the 64 that loading the MFMA
+// fragments directly would touch) into a wave-private LDS area, stored in
+// fragment order [step][lane][16 B] with the lane slot XOR-ed by 4 * step
+// (conflict-free writes and reads; LDS operations of one wave complete in
+// order, so no barrier is needed). With XLDS false (a few activation rows,
+// where nearly all lanes of such a load would be out of range anyway) each
+// lane loads its fragments directly. Offsets past the last chunk or row get
+// the top bit set and read zeros.
+template <int MT, int NP, int NW, int D, bool XLDS>
+__global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int XS = 8192;  // one 32-row block of one chunk: 32 rows x 256 B
+  constexpr int RED = NW * MT * 4096;  // one panel's partial tiles of all waves
+  constexpr int STG = XLDS ? NW * MT * XS : 0;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[STG > RED ? STG : RED];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int panel = blockIdx.x;
+  const int mb = blockIdx.y * 32 * MT;
   const int kcn = g.k >> 7;
   const int r = lane & 31, gq = lane >> 5;
-  const uint16_t* x = reinterpret_cast<const uint16_t*>(g.a);
-  v16f acc[MT];
+  const int npanels_w = (g.n + 31) >> 5;
+  const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 2048), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a), 0, (int)(((int64_t)(g.m - 1) * g.lda + g.k) * 2), 0x00020000);
+  uint32_t ow[NP], ows[NP];
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+  for (int j = 0; j < NP; ++j) {
+    const int pj = panel * NP + j;
+    const bool in = pj < npanels_w;
+    ow[j] = in ? (uint32_t)(pj * kcn * 2048 + lane * 16) : OOB;
+    ows[j] = in ? (uint32_t)(pj * kcn * 256 + r * 8 + 4 * gq) : OOB;
+  }
+  // row-contiguous activation pieces: load it covers rows 4 it .. 4 it + 3 of
+  // the block; lane -> row 4 it + lane / 16, piece c = lane % 16 (elements
+  // 8c .. 8c + 7 of the chunk) = step c % 8 of lane half c / 8
+  // (direct: lane loads elements [64 g + 8 s, +8) of row r at step s)
+  const int prow = XLDS ? (lane >> 4) : r, pc = XLDS ? (lane & 15) : 8 * gq;
+  uint32_t ox[MT];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[i][v] = 0.0f;
-  for (int kc = wave; kc < kcn; kc += NW) {
-    const int64_t chunk = (int64_t)panel * kcn + kc;
-    const uint4 c0 = reinterpret_cast<const uint4*>(g.w_codes + chunk * 2048)[lane];
-    const uint4 c1 = reinterpret_cast<const uint4*>(g.w_codes + chunk * 2048 + 1024)[lane];
-    const uint32_t sc = *reinterpret_cast<const uint32_t*>(g.w_scales + chunk * 256 + r * 8 + 4 * gq);
-    const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+  for (int i = 0; i < MT; ++i) {
+    const int row = mb + 32 * i + prow;  // + 4 it when staged
+    ox[i] = (row < g.m) ? (uint32_t)(((int64_t)row * g.lda + 8 * pc) * 2) : OOB;
+  }
+  const uint32_t xrow4 = (uint32_t)(4 * g.lda * 2);  // bytes per 4 rows
+  const int srow_lim = g.m - mb - prow;               // rows of the block this lane may read: 4 it < srow_lim
+  uint8_t* xw = smem + wave * MT * XS;
+  // piece (row 4 it + prow, c) belongs to lane slot (row + 32 g) of step
+  // s = c % 8, g = c / 8, stored at slot ^ 4s: 4 (it ^ s) + prow + 32 g
+  const int ps = pc & 7;
+  const int wbase = ps * 1024 + (prow + 32 * (pc >> 3)) * 16;
+
+  struct Chunk {
+    v4i c0[NP], c1[NP];  // 64 E2M1 codes of the lane's row of each weight panel
+    uint32_t sc[NP];     // their 4 E4M3 block scales
+    v4i x[MT][8];        // row-contiguous activation pieces
+  };
+  auto load = [&](Chunk& C, int kc) __attribute__((always_inline)) {
+    const uint32_t hi = kc < kcn ? 0u : OOB;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      C.c0[j] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 2048) | hi, 0, 0);
+      C.c1[j] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 2048 + 1024) | hi, 0, 0);
+      C.sc[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, (ows[j] + kc * 256) | hi, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        if (XLDS) {
+          const uint32_t rowhi = (4 * it < srow_lim - 32 * i) ? 0u : OOB;
+          C.x[i][it] = __builtin_amdgcn_raw_buffer_load_b128(rs_x, (ox[i] + it * xrow4 + kc * 256) | hi | rowhi, 0, 0);
+        } else {
+          C.x[i][it] = __builtin_amdgcn_raw_buffer_load_b128(rs_x, (ox[i] + it * 16 + kc * 256) | hi, 0, 0);
+        }
+      }
+  };
+  v16f acc[NP][MT];
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.0f;
+  auto compute = [&](const Chunk& C) __attribute__((always_inline)) {
+    if (XLDS) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int it = 0; it < 8; ++it)
+          *reinterpret_cast<v4i*>(xw + i * XS + wbase + 64 * (it ^ ps)) = C.x[i][it];
+    }
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      const v8bf wb = __builtin_bit_cast(v8bf, dequant8_bf16(cw[s], dec_e4m3((sc >> (8 * (s >> 1))) & 0xFFu)));
+      v4i xf[MT];
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        const int m = 32 * i + r;
-        v4i xv = {0, 0, 0, 0};
-        if (m < g.m) xv = *reinterpret_cast<const v4i*>(x + (int64_t)m * g.lda + kc * 128 + 64 * gq + 8 * s);
-        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb, __builtin_bit_cast(v8bf, xv), acc[i], 0, 0, 0);
+      for (int i = 0; i < MT; ++i)
+        xf[i] = XLDS ? *reinterpret_cast<const v4i*>(xw + i * XS + s * 1024 + ((lane ^ (4 * s)) * 16)) : C.x[i][s];
+#pragma unroll
+      for (int j = 0; j < NP; ++j) {
+        const v4i cc = (s < 4) ? C.c0[j] : C.c1[j];
+        const uint32_t w = (uint32_t)((s & 3) == 0 ? cc.x : (s & 3) == 1 ? cc.y : (s & 3) == 2 ? cc.z : cc.w);
+        const v8bf wb = __builtin_bit_cast(v8bf, dequant8_bf16(w, dec_e4m3_scale(C.sc[j] >> (8 * (s >> 1)))));
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb, __builtin_bit_cast(v8bf, xf[i]), acc[j][i], 0, 0, 0);
+      }
+    }
+  };
+  // a wave's chunks kc = wave + NW t are loaded D at a time, all D before any
+  // is used, so a short reduction costs one memory latency
+  for (int base = wave; base < kcn; base += D * NW) {
+    Chunk C[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) load(C[d], base + d * NW);
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (base + d * NW < kcn) compute(C[d]);
+  }
+
+  // sum the NW partial tiles through LDS (the staging area is reused after a
+  // barrier), one panel at a time: thread t owns 4 consecutive outputs
+  // (tile i, lane l, quad q) and writes them as one 8-byte bf16 store
+  float* red = reinterpret_cast<float*>(smem);  // [NW][MT][64][16]
+  const float c = *g.w_tscale;
+#pragma unroll
+  for (int j = 0; j < NP; ++j) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(red + ((wave * MT + i) * 64 + lane) * 16 + 4 * q) =
+            make_float4(acc[j][i][4 * q], acc[j][i][4 * q + 1], acc[j][i][4 * q + 2], acc[j][i][4 * q + 3]);
+    __syncthreads();
+    for (int t = threadIdx.x; t < MT * 256; t += 64 * NW) {
+      const int i = t >> 8, l = (t >> 2) & 63, q = t & 3;
+      float4 sum = *reinterpret_cast<const float4*>(red + (i * 64 + l) * 16 + 4 * q);
+#pragma unroll
+      for (int w = 1; w < NW; ++w) {
+        const float4 v = *reinterpret_cast<const float4*>(red + ((w * MT + i) * 64 + l) * 16 + 4 * q);
+        sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+      }
+      const int m = mb + 32 * i + (l & 31);
+      const int n = (panel * NP + j) * 32 + 8 * q + 4 * (l >> 5);
+      if (m >= g.m || n >= g.n) continue;
+      const float v0 = sum.x * c, v1 = sum.y * c, v2 = sum.z * c, v3 = sum.w * c;
+      if (g.f32out) {
+        float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+        if ((reinterpret_cast<uintptr_t>(o) & 15) == 0) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
+        else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
+      } else {
+        uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+        const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
+        if ((reinterpret_cast<uintptr_t>(o) & 7) == 0) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
+        else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
       }
     }
   }
-  __shared__ v16f red[NW][MT][64];
-#pragma unroll
-  for (int i = 0; i < MT; ++i) red[wave][i][lane] = acc[i];
+}
+
+// W4A16 with very few activation rows against a wide weight (a weight pool
+// streamed once): HBM-bound, so the weight stream is all that matters. A
+// persistent workgroup stages the activation rows in LDS once (row pitch
+// padded by 16 bytes, so that the rows of a fragment read fall in different
+// banks); each of its waves then owns whole 32-row weight panels (no split
+// of the reduction, no cross-wave reduction), walking the panel's chunks in
+// groups of D with the next group's weight loads issued before the current
+// group's MFMAs, so every wave keeps D chunks (D x 2.3 KiB) in flight.
+// Lanes of activation rows past m read an extra all-zero row. Requires
+// m <= 32 and (m + 1) rows within the LDS budget (checked by the launcher).
+template <int D>
+__global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
+  constexpr uint32_t OOB = 0x80000000u;
+  extern __shared__ __attribute__((aligned(16))) uint8_t xl[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 31, gq = lane >> 5;
+  const int kcn = g.k >> 7;
+  const int npan = (g.n + 31) >> 5;
+  const int pitch = g.k * 2 + 16;
+  // stage the activation rows and one zero row (16 bytes per thread and step)
+  {
+    const int pieces = g.k >> 3;  // 16-byte pieces per row
+    for (int t = threadIdx.x; t < (g.m + 1) * pieces; t += 512) {
+      const int row = t / pieces, c = t - row * pieces;
+      *reinterpret_cast<uint4*>(xl + row * pitch + c * 16) =
+          (row < g.m) ? *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(g.a) + (int64_t)row * g.lda + 8 * c)
+                      : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
   __syncthreads();
-  if (wave != 0) return;
+  const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npan * kcn * 2048), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npan * kcn * 256), 0x00020000);
+  const uint8_t* xrd = xl + min(r, g.m) * pitch + 128 * gq;  // + kc * 256 + s * 16
   const float c = *g.w_tscale;
+  struct W { v4i c0, c1; uint32_t sc; };
+  W buf[2][D];
+  auto load = [&](W (&b)[D], int panel, int kc0) __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    v16f t = red[0][i][lane];
+    for (int d = 0; d < D; ++d) {
+      const int kc = kc0 + d;
+      const uint32_t o = (kc < kcn && panel < npan) ? (uint32_t)((panel * kcn + kc) * 2048 + lane * 16) : OOB;
+      const uint32_t os = (kc < kcn && panel < npan) ? (uint32_t)((panel * kcn + kc) * 256 + r * 8 + 4 * gq) : OOB;
+      b[d].c0 = __builtin_amdgcn_raw_buffer_load_b128(rs_w, o, 0, 0);
+      b[d].c1 = __builtin_amdgcn_raw_buffer_load_b128(rs_w, o + 1024, 0, 0);
+      b[d].sc = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, os, 0, 0);
+    }
+  };
+  v16f acc;
+  auto compute = [&](const W (&b)[D], int kc0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int w = 1; w < NW; ++w) t += red[w][i][lane];
-    const int m = 32 * i + r;
-    if (m >= g.m) continue;
+    for (int d = 0; d < D; ++d) {
+      if (kc0 + d >= kcn) break;
+      const uint32_t cw[8] = {(uint32_t)b[d].c0.x, (uint32_t)b[d].c0.y, (uint32_t)b[d].c0.z, (uint32_t)b[d].c0.w,
+                              (uint32_t)b[d].c1.x, (uint32_t)b[d].c1.y, (uint32_t)b[d].c1.z, (uint32_t)b[d].c1.w};
 #pragma unroll
-    for (int qd = 0; qd < 4; ++qd) {
-      const int n = panel * 32 + 8 * qd + 4 * gq;
-      if (n >= g.n) continue;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float v = t[4 * qd + e] * c;
-        if (g.f32out) reinterpret_cast<float*>(g.y)[(int64_t)m * g.ldy + n + e] = v;
-        else reinterpret_cast<uint16_t*>(g.y)[(int64_t)m * g.ldy + n + e] = (uint16_t)f32_to_bf16(v);
+      for (int s = 0; s < 8; ++s) {
+        const v8bf wb = __builtin_bit_cast(v8bf, dequant8_bf16(cw[s], dec_e4m3_scale(b[d].sc >> (8 * (s >> 1)))));
+        const v4i xv = *reinterpret_cast<const v4i*>(xrd + (kc0 + d) * 256 + s * 16);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb, __builtin_bit_cast(v8bf, xv), acc, 0, 0, 0);
       }
     }
+  };
+  const int nw = gridDim.x * 8;
+  int panel = blockIdx.x * 8 + wave;
+  int kc0 = 0, cur = 0;
+  if (panel < npan) load(buf[0], panel, 0);
+  while (panel < npan) {
+    // the group after this one: next chunks of this panel, or the next panel
+    int np_ = panel, nk = kc0 + D;
+    if (nk >= kcn) { np_ = panel + nw; nk = 0; }
+    if (kc0 == 0)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+    if (cur == 0) { load(buf[1], np_, nk); compute(buf[0], kc0); }
+    else { load(buf[0], np_, nk); compute(buf[1], kc0); }
+    cur ^= 1;
+    if (nk == 0) {
+      // panel done: lane (r, g) holds rows r of columns 8q + 4g + e
+      const int m = r;
+      if (m < g.m) {
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int n = panel * 32 + 8 * qd + 4 * gq;
+          if (n >= g.n) continue;
+          const float v0 = acc[4 * qd] * c, v1 = acc[4 * qd + 1] * c, v2 = acc[4 * qd + 2] * c, v3 = acc[4 * qd + 3] * c;
+          if (g.f32out) {
+            float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+            o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3;
+          } else {
+            uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+            const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
+            o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16);
+          }
+        }
+      }
+    }
+    panel = np_;
+    kc0 = nk;
   }
 }
 
@@ -1316,13 +1537,30 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
     return hipGetLastError();
   } else {
-    if (m <= 64) {
-      const unsigned grid = (unsigned)((n + 31) / 32);
-      if (m <= 32) hipLaunchKernelGGL((k_w4a16_skinny<1, 8>), dim3(grid), dim3(512), 0, st, g);
-      else hipLaunchKernelGGL((k_w4a16_skinny<2, 8>), dim3(grid), dim3(512), 0, st, g);
+    const int64_t npan_all = (n + 31) / 32;
+    const int64_t xbytes = (m + 1) * (k * 2 + 16);
+    if (m <= 16 && npan_all >= 8 * (int64_t)device_cus() && xbytes <= 128 * 1024) {
+      const unsigned grid = (unsigned)std::min<int64_t>(device_cus(), (npan_all + 7) / 8);
+      hipLaunchKernelGGL((k_w4a16_stream<6>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
       return hipGetLastError();
     }
-    if (m <= 1024) return run<MODE_W4A16, 2, 2, 1, 2>(g, st);
+    if (m <= 1024) {
+      // Shapes measured on the MI355X (text-encoder linears, M <= 512):
+      // one-panel workgroups of 8 waves for narrow outputs; two panels per
+      // 4-wave workgroup once the output is wide enough that the activation
+      // re-reads (once per workgroup column) dominate.
+      const int64_t npan = (n + 31) / 32;
+      const unsigned mt = (unsigned)((m + 31) / 32);
+      if (n >= 2048 && m > 32)
+        hipLaunchKernelGGL((k_w4a16_splitk<1, 2, 4, 3, true>), dim3((unsigned)((npan + 1) / 2), mt), dim3(256), 0, st, g);
+      else if (m <= 32)
+        hipLaunchKernelGGL((k_w4a16_splitk<1, 1, 8, 3, false>), dim3((unsigned)npan, mt), dim3(512), 0, st, g);
+      else if (m <= 256)
+        hipLaunchKernelGGL((k_w4a16_splitk<1, 1, 8, 3, true>), dim3((unsigned)npan, mt), dim3(512), 0, st, g);
+      else
+        hipLaunchKernelGGL((k_w4a16_splitk<1, 2, 8, 3, true>), dim3((unsigned)((npan + 1) / 2), mt), dim3(512), 0, st, g);
+      return hipGetLastError();
+    }
     return run<MODE_W4A16, 2, 2, 2, 4>(g, st);
   }
 }

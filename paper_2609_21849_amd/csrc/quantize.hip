@@ -72,6 +72,35 @@ __global__ void __launch_bounds__(256) k_amax_partial(const uint16_t* __restrict
     partial[blockIdx.y * gridDim.x + blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
 }
 
+// Dense, 16-byte aligned tensors of `units` 8-element units: workgroup w
+// covers units [2048 w, 2048 w + 2048) as eight wave-contiguous runs and each
+// thread issues all eight of its 16-byte loads before the first max, so the
+// whole tensor is in flight at once instead of a few loads per thread.
+__global__ void __launch_bounds__(256) k_amax_dense(const uint16_t* __restrict__ x, int64_t units,
+                                                    uint32_t* __restrict__ partial) {
+  constexpr int U = 8;
+  const uint4* xv = reinterpret_cast<const uint4*>(x);
+  const int64_t base = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
+  uint4 v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) v[u] = (base + u * 256 < units) ? xv[base + u * 256] : make_uint4(0u, 0u, 0u, 0u);
+  uint32_t m = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t t = w[i] & 0x7FFF7FFFu;
+      m = max(m, max(t & 0xFFFFu, t >> 16));
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
+}
+
 // Max of `count` partials (bf16 magnitude bits) -> decode scale, written to
 // `slot`. divisor = 448 (FP8) or 2688 = 448 * 6 (NVFP4). Inf/NaN anywhere in
 // the tensor leaves a NaN scale as the sentinel. `partial` may be `slot`
@@ -192,30 +221,37 @@ __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict_
 
 // ---------------------------------------------------------------- dense tensors
 // Dense tensors (ldx == cols, 16-byte aligned rows): each wavefront codes a
-// chunk of 1024 consecutive elements. Lane l reads elements [8l, 8l + 8) and
-// [512 + 8l, 512 + 8l + 8) of the chunk with one 16-byte load each, so every
-// load and store instruction of the wave covers one contiguous run of memory.
-// Elements are coded with the hardware conversions (hw_e4m3x4 / hw_e2m1x8).
-// NVFP4: n % 16 == 0, so lanes (2j, 2j+1) hold one whole 16-element block
-// (or both lie past the end); the block max is shared with one lane swap.
-template <int FMT>
+// chunk of 512 H consecutive elements. Lane l reads elements
+// [512 h + 8l, 512 h + 8l + 8) of the chunk for h < H with one 16-byte load
+// each, all issued before the first is used, so every load and store
+// instruction of the wave covers one contiguous run of memory and H loads
+// per lane are in flight. Elements are coded with the hardware conversions
+// (hw_e4m3x4 / hw_e2m1x8). NVFP4: n % 16 == 0, so lanes (2j, 2j+1) hold one
+// whole 16-element block (or both lie past the end); the block max is shared
+// with one lane swap.
+template <int FMT, int H>
 __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict__ x, int64_t n,
                                                      uint8_t* __restrict__ q,
                                                      uint8_t* __restrict__ bscale,
                                                      const float* __restrict__ tscale) {
   const int lane = threadIdx.x & 63;
   const int64_t chunk = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+  uint4 raw[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
+    raw[h] = (e0 + 8 <= n) ? *reinterpret_cast<const uint4*>(x + e0) : make_uint4(0u, 0u, 0u, 0u);
+  }
   const float s = *tscale;
   const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
   const float d_t = __fmul_rn(6.0f, s);
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int64_t e0 = chunk * 1024 + h * 512 + lane * 8;
+  for (int h = 0; h < H; ++h) {
+    const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
     const bool full = (e0 + 8 <= n);
     float v[8];
     if (full) {
-      const uint4 w = *reinterpret_cast<const uint4*>(x + e0);
-      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+      const uint32_t ww[4] = {raw[h].x, raw[h].y, raw[h].z, raw[h].w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         v[2 * j] = bf16_lo(ww[j]);
@@ -344,28 +380,36 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
     const int64_t code_bytes = (fmt == 1) ? rows * cols : rows * cols / 2;
     const uintptr_t base = (reinterpret_cast<uintptr_t>(codes) + 3) & ~uintptr_t(3);
     const int64_t cap = (code_bytes - (int64_t)(base - reinterpret_cast<uintptr_t>(codes))) / 4;
-    int64_t gy = std::min<int64_t>(r_eff, 1024);
-    int64_t gx = std::min<int64_t>(std::max<int64_t>(1, (per_row + 1023) / 1024), std::max<int64_t>(1, 1024 / gy));
+    int64_t gx, gy;
     uint32_t* partial = reinterpret_cast<uint32_t*>(base);
-    if (gx * gy > cap) {   // tiny tensor: one workgroup, its max goes straight to the scale slot
-      gx = gy = 1;
-      partial = reinterpret_cast<uint32_t*>(tscale);
+    const int64_t dense_groups = (c_eff / 8 + 2047) / 2048;
+    if (contig && vec && dense_groups <= cap) {
+      gx = dense_groups;
+      gy = 1;
+      hipLaunchKernelGGL(k_amax_dense, dim3((unsigned)gx), dim3(256), 0, st, x, c_eff / 8, partial);
+    } else {
+      gy = std::min<int64_t>(r_eff, 1024);
+      gx = std::min<int64_t>(std::max<int64_t>(1, (per_row + 1023) / 1024), std::max<int64_t>(1, 1024 / gy));
+      if (gx * gy > cap) {  // tiny tensor: one workgroup, its max goes straight to the scale slot
+        gx = gy = 1;
+        partial = reinterpret_cast<uint32_t*>(tscale);
+      }
+      if (vec)
+        hipLaunchKernelGGL(k_amax_partial<true>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
+                           contig ? c_eff : ldx, partial);
+      else
+        hipLaunchKernelGGL(k_amax_partial<false>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
+                           contig ? c_eff : ldx, partial);
     }
-    if (vec)
-      hipLaunchKernelGGL(k_amax_partial<true>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
-                         contig ? c_eff : ldx, partial);
-    else
-      hipLaunchKernelGGL(k_amax_partial<false>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, st, x, r_eff, c_eff,
-                         contig ? c_eff : ldx, partial);
     hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, st, partial, (int)(gx * gy), tscale,
                        fmt == 1 ? 448.0f : 2688.0f);
   }
   const int64_t n = rows * cols;
   const bool qal = (reinterpret_cast<uintptr_t>(codes) % 8 == 0);
   if (contig && aligned && qal) {
-    const unsigned g = (unsigned)((n + 4095) / 4096);  // 4 waves x 1024 elements per workgroup
-    if (fmt == 1) hipLaunchKernelGGL(k_quant_dense<1>, dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
-    else hipLaunchKernelGGL(k_quant_dense<2>, dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+    const unsigned g = (unsigned)((n + 8191) / 8192);  // 4 waves x 2048 elements per workgroup
+    if (fmt == 1) hipLaunchKernelGGL((k_quant_dense<1, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+    else hipLaunchKernelGGL((k_quant_dense<2, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
   } else if (fmt == 1) {
     const bool qal16 = (reinterpret_cast<uintptr_t>(codes) % 16 == 0);
     if (contig) {

@@ -35,7 +35,8 @@ def run_linear(kind, x, w, out=q.QG_OUT_BF16, check_codes=True):
 
 @pytest.mark.parametrize("kind", ["fp8", "nvfp4", "w4a16"])
 @pytest.mark.parametrize("m,n,k", [(1, 16, 128), (17, 48, 256), (64, 256, 256), (65, 128, 128),
-                                   (300, 272, 384), (257, 512, 1024), (512, 768, 640)])
+                                   (300, 272, 384), (257, 512, 1024), (512, 768, 640), (100, 2080, 384),
+                                   (129, 528, 1152)])
 @pytest.mark.parametrize("out", [q.QG_OUT_F32, q.QG_OUT_BF16])
 def test_small_full_parity(kind, m, n, k, out):
     log("gemm kind=%s m=%d n=%d k=%d out=%d" % (kind, m, n, k, out))
@@ -191,3 +192,18 @@ def test_w4a16_encoder_full(name, m):
     w = synth.normal_bf16(n, k, 0.02, 0, 1)
     y = run_linear("w4a16", x, w)
     log("w4a16 %s m=%d max err/B" % (name, m), check_linear(y, oracle.linear_reference("w4a16", x, w)))
+
+
+@pytest.mark.parametrize("m,k", [(1, 1024), (7, 1024), (16, 1024), (15, 3072)])
+def test_w4a16_weight_pool_sampled(m, k):
+    # a few activation rows against a very wide weight (a pool of stacked
+    # encoder weights streamed once): the persistent streaming kernel, with a
+    # ragged last panel group; sampled outputs against the oracle
+    n = 70016
+    log("w4a16 pool m=%d n=%d k=%d" % (m, n, k))
+    x = synth.normal_bf16(m, k, 1.0, 5, 0)
+    w = synth.normal_bf16(n, k, 0.02, 5, 1)
+    y = run_linear("w4a16", x, w)
+    rows, cols = _sample(m, n, 2000, 3)
+    ref = oracle.linear_reference("w4a16", x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))

@@ -44,7 +44,133 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-mib", type=int, default=600,
                     help="size of the weight pool for the cold-HBM W4A16 measurement")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="only launch the dominant GEMM (3x per DiT shape) and a calibration copy; "
+                         "for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT_MD"),
+                    help="turn the two counter runs of --traffic-probe into the traffic summary")
     return ap.parse_args()
+
+
+# HBM traffic of the dominant kernel, measured with rocprofv3 counters (see
+# --traffic-probe / --traffic-summary) and kept as a text summary; reported
+# only while the kernel source is the one the counters were taken on.
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "k_gemm_nvfp4_direct_dit_traffic.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_21849_amd", "csrc", "gemm.hip")
+COPY_BYTES = 512 * 2 ** 20
+
+
+def source_sha() -> str:
+    import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def nvfp4_gemm_bytes(m, n, k):
+    """Algorithmic bytes of one W4A4 GEMM: A codes + scales, packed W codes +
+    scales, bf16 Y."""
+    return m * k * (0.5 + 1 / 16) + n * k * (0.5 + 1 / 16) + 2 * m * n
+
+
+def traffic_probe():
+    import torch
+    import paper_2609_21849_amd as q
+    import synth
+    torch.cuda.set_device(0)
+    M = synth.DIT_TOKENS
+    runs = []
+    for li, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
+        base = 16 * li
+        x = synth.normal_bf16(M, k, synth.SIGMA_X, 0, base + synth.STREAM_X,
+                              outlier_frac=synth.HEAVY_TAIL_FRAC, outlier_gain=synth.HEAVY_TAIL_GAIN,
+                              outlier_stream=base + synth.STREAM_OUTLIER)
+        w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
+        a = q.quantize(dev_bf16(x), q.QG_FMT_NVFP4)
+        p = q.pack(q.quantize(dev_bf16(w), q.QG_FMT_NVFP4))
+        y = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
+        runs.append((a, p, y, n))
+    torch.cuda.synchronize()
+    for a, p, y, n in runs:
+        for _ in range(3):
+            q.linear(a, p, q.QG_FMT_NVFP4, n, y=y)
+    torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print("traffic probe done", flush=True)
+
+
+def traffic_summary(fetch_dir, write_dir, out_md):
+    import csv
+    import glob
+    import synth
+
+    def read(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rows += [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r.get("Dispatch_Id", 0)))
+        gemm = [float(r["Counter_Value"]) for r in rows if "k_gemm_nvfp4_direct" in r["Kernel_Name"]]
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
+                or "copy_kernel" in r["Kernel_Name"]]
+        return gemm, copy
+
+    fg, fc = read(fetch_dir, "FETCH_SIZE")
+    wg, wc = read(write_dir, "WRITE_SIZE")
+    assert len(fg) == len(wg) == 12 and fc and wc, (len(fg), len(wg), len(fc), len(wc))
+    f_factor = (sum(fc) / len(fc)) * 1024 / COPY_BYTES   # counter KiB per true byte, x1024
+    w_factor = (sum(wc) / len(wc)) * 1024 / COPY_BYTES
+    M = synth.DIT_TOKENS
+    shapes = list(synth.DIT_LINEARS.items())
+    per = []
+    for i, (name, (n, k)) in enumerate(shapes):
+        fb = sum(fg[3 * i:3 * i + 3]) / 3 * 1024 / f_factor
+        wb = sum(wg[3 * i:3 * i + 3]) / 3 * 1024 / w_factor
+        per.append({"linear": name, "m": M, "n": n, "k": k, "fetch_bytes": round(fb), "write_bytes": round(wb),
+                    "algorithmic_bytes": round(nvfp4_gemm_bytes(M, n, k))})
+    t = sum(p["fetch_bytes"] + p["write_bytes"] for p in per) / len(per)
+    alg = sum(p["algorithmic_bytes"] for p in per) / len(per)
+    data = {"kernel": "k_gemm_nvfp4_direct", "source": "paper_2609_21849_amd/csrc/gemm.hip",
+            "source_sha": source_sha(), "traffic_bytes_per_launch": round(t),
+            "algorithmic_bytes_per_launch": round(alg), "ratio": round(t / alg, 3),
+            "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib": sum(fc) / len(fc), "write_kib": sum(wc) / len(wc),
+                                 "fetch_factor": round(f_factor, 4), "write_factor": round(w_factor, 4)},
+            "per_shape": per}
+    lines = ["# HBM traffic of k_gemm_nvfp4_direct at the DiT shapes (M = 4608)", "",
+             "Commands (from the repository root on the MI355X box):", "",
+             "```",
+             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py --traffic-probe",
+             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py --traffic-probe",
+             "python3 bench.py --traffic-summary gpurun_out/pmc_fetch gpurun_out/pmc_write <this file>",
+             "```", "",
+             "Each counter is scaled by what it reads for a %d MiB device-to-device copy (%d MiB read, %d MiB "
+             "written): fetch factor %.4f, write factor %.4f (counter KiB x 1024 / true bytes)."
+             % (COPY_BYTES >> 20, COPY_BYTES >> 20, COPY_BYTES >> 20, f_factor, w_factor), "",
+             "| linear | N | K | fetch MB | write MB | algorithmic MB |", "|---|---|---|---|---|---|"]
+    for p in per:
+        lines.append("| %s | %d | %d | %.1f | %.1f | %.1f |" % (p["linear"], p["n"], p["k"], p["fetch_bytes"] / 1e6,
+                                                              p["write_bytes"] / 1e6, p["algorithmic_bytes"] / 1e6))
+    lines += ["", "Per launch (mean of the four shapes): %.1f MB measured vs %.1f MB algorithmic (ratio %.3f)."
+              % (t / 1e6, alg / 1e6, t / alg), "", "```json", json.dumps(data, indent=1), "```", ""]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines))
+    print(json.dumps(data))
+
+
+def recorded_traffic():
+    """(bytes per launch, summary) of the committed traffic summary, or
+    (None, reason) when it is missing or was taken on another kernel source."""
+    try:
+        txt = open(TRAFFIC_MD).read()
+        blob = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, IndexError, ValueError):
+        return None, "no traffic summary"
+    if blob.get("source_sha") != source_sha():
+        return None, "kernel source changed since the counters were taken"
+    return blob["traffic_bytes_per_launch"], blob
 
 
 def dev_bf16(bits):
@@ -54,6 +180,12 @@ def dev_bf16(bits):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
+    if args.traffic_probe:
+        traffic_probe()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path "
               "(column/token sharding is a design note only); run with --gpus 1", file=sys.stderr)
@@ -206,9 +338,13 @@ def main():
     dur_ms = sum(d for _, d in launches)
     achieved = fl / (dur_ms * 1e9)  # TFLOP/s
     peak = PEAK["fp8"] if dom == "fp8" else PEAK["f16"]
-    roofline = {"bound": "mfma", "kernel": "k_gemm<%s>" % ("W8A8 fp8 MFMA" if dom == "fp8" else "W4A4 fp16 MFMA"),
+    traffic, tinfo = recorded_traffic() if dom == "nvfp4" else (None, "counters taken for the W4A4 kernel only")
+    roofline = {"bound": "mfma",
+                "kernel": "k_gemm_fp8_direct (W8A8, fp8 MFMA)" if dom == "fp8" else "k_gemm_nvfp4_direct (W4A4, fp16 MFMA)",
                 "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None,
+                "frac": round(achieved / peak, 4), "traffic": traffic,
+                "traffic_note": ("HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated), "
+                                 "algorithmic %d" % tinfo["algorithmic_bytes_per_launch"]) if traffic else tinfo,
                 "avg_launch_us": round(1e3 * dur_ms / len(launches), 2), "launches": len(launches),
                 "flops_per_launch_avg": fl / len(launches)}
 

@@ -328,6 +328,7 @@ def main():
                    "tflops": round(flops(e, e["m"]) / (ms * 1e9), 2)}
     parts["w4a16_single_call"] = w4
     parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
+    parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
     parts["w4a16_cold_pool"] = w4a16_pool(q, synth, args.pool_mib)
 
     # dominant kernel: the GEMM kind with the largest share of the step
@@ -367,6 +368,50 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def static_scale_part(q, lib, st, dit, M, flops, steps=10):
+    """The same DiT linears with static (calibrated) activation scales: one
+    quantize kernel + the GEMM per linear. The calibrated scale used here is
+    the one the dynamic pass derived for the same activations, so the codes
+    (and the GEMMs) are those of the dynamic step."""
+    import torch
+    plan = []
+    for kind, fmt in (("fp8", q.QG_FMT_FP8_E4M3), ("nvfp4", q.QG_FMT_NVFP4)):
+        for e in dit:
+            a, x, wp, y = e["a_" + kind], e["x"][kind], e["w_" + kind], e["y_" + kind]
+            s_cal = a.tensor_scale.clone()
+            bs = a.block_scales.data_ptr() if a.block_scales is not None else None
+            plan.append((("squant", kind, e["name"]), lib.qg_quantize_act_static,
+                         (fmt, x.data_ptr(), M, e["k"], e["k"], a.codes.data_ptr(), bs, s_cal.data_ptr(), st)))
+            plan.append((("gemm", kind, e["name"]), lib.qg_gemm,
+                         (fmt, a.codes.data_ptr(), bs, s_cal.data_ptr(), e["k"], fmt,
+                          wp.data_ptr(), wp.numel(), M, e["n"], e["k"], y.data_ptr(), e["n"],
+                          q.QG_OUT_BF16, st)))
+            e.setdefault("keep", []).append(s_cal)
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plan]
+           for _ in range(steps + 2)]
+    for i in range(steps + 2):
+        for (key, fn, fargs), (s0, s1) in zip(plan, evs[i]):
+            s0.record()
+            rc = fn(*fargs)
+            s1.record()
+            if rc != 0:
+                raise q.QGError(rc, str(key))
+    torch.cuda.synchronize()
+    dur = {}
+    for i in range(2, steps + 2):
+        for (key, _, _), (s0, s1) in zip(plan, evs[i]):
+            dur.setdefault(key, []).append(s0.elapsed_time(s1))
+    out = {}
+    for kind in ("fp8", "nvfp4"):
+        qms = sum(float(np.mean(dur[("squant", kind, e["name"])])) for e in dit)
+        gms = sum(float(np.mean(dur[("gemm", kind, e["name"])])) for e in dit)
+        f = sum(flops(e) for e in dit)
+        out[kind] = {"quant_us": {e["name"]: round(1e3 * float(np.mean(dur[("squant", kind, e["name"])])), 2)
+                                  for e in dit},
+                     "linear_tflops_incl_quant": round(f / ((gms + qms) * 1e9), 1)}
+    return out
 
 
 def w4a16_pool(q, synth, pool_mib):

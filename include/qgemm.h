@@ -101,6 +101,28 @@ qg_status qg_quantize_act(qg_format fmt, const void *x, int64_t rows, int64_t co
                           void *codes, void *block_scales, float *tensor_scale, void *stream);
 
 /*
+ * qg_quantize_act_static -- quantization of a bf16 tensor with a static
+ * (calibrated) decode scale instead of the tensor's own max: post-training
+ * quantization with fixed activation ranges, which removes the tensor-wide
+ * max reduction (two of the three kernels of qg_quantize_act) from the run
+ * time. Paper: Sec. 4, quantization paragraph (PTQ recipe).
+ *
+ *   fmt, x, rows, cols, ldx, codes, block_scales: as for qg_quantize_act.
+ *   tensor_scale  in: the fp32 decode scale (FP8: s; NVFP4: s_t), e.g. the
+ *                 value qg_quantize_act wrote for calibration data, or the
+ *                 max of such values over several batches. It must be 0 or
+ *                 a normal positive number (FP8), 0 or >= 2^-96 (NVFP4);
+ *                 other values give unspecified codes. It is not written.
+ * Arithmetic: the element (and, for NVFP4, block) steps of qg_quantize_act
+ * with the given scale; elements beyond the calibrated range saturate to
+ * +-448 (FP8) or to a block scale of 448 and codes of +-6 (NVFP4). With the
+ * scale qg_quantize_act would derive, the codes are identical to its codes.
+ * An empty tensor enqueues nothing.
+ */
+qg_status qg_quantize_act_static(qg_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                                 void *codes, void *block_scales, const float *tensor_scale, void *stream);
+
+/*
  * qg_packed_bytes -- size of the packed weight buffer for an [n, k] weight
  * in `fmt` (FP8 or NVFP4), or 0 when the shape breaks the GEMM contract
  * (n % 16, k % 128) or the format is not packable.
@@ -150,6 +172,9 @@ qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_byt
  * are applied once at the end), then rounded to y_dtype. Accuracy contract:
  * |y - y_exact| <= 1e-3 * sum_k |a w| plus the rounding of y to y_dtype.
  * Shapes: m, n, k >= 0; n % 16 == 0; k % 128 == 0; lda >= k, ldy >= n.
+ * Operands are addressed with 32-bit byte offsets: the activation extent
+ * ((m - 1) * lda + k elements), NVFP4 activation scales and the packed
+ * weight must each stay below 2 GiB, else QG_ERR_SHAPE.
  */
 qg_status qg_gemm(qg_format a_fmt, const void *a, const void *a_block_scales,
                   const float *a_tensor_scale, int64_t lda,

@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
         L.qo_quantize_fp8.argtypes = [P, I64, I64, I64, P, P]
         L.qo_quantize_nvfp4.restype = ctypes.c_int
         L.qo_quantize_nvfp4.argtypes = [P, I64, I64, I64, P, P, P]
+        L.qo_quantize_fp8_static.restype = ctypes.c_int
+        L.qo_quantize_fp8_static.argtypes = [P, I64, I64, I64, ctypes.c_float, P]
+        L.qo_quantize_nvfp4_static.restype = ctypes.c_int
+        L.qo_quantize_nvfp4_static.argtypes = [P, I64, I64, I64, ctypes.c_float, P, P]
         L.qo_dequant_fp8_f64.argtypes = [P, I64, ctypes.c_float, P]
         L.qo_dequant_nvfp4_f64.argtypes = [P, P, I64, I64, ctypes.c_float, P]
         L.qo_dequant_fp8_f32.argtypes = [P, I64, ctypes.c_float, P]
@@ -236,6 +240,38 @@ def num_threads() -> int:
 
 
 # ---------------------------------------------------------------- end-to-end references
+def quantize_fp8_static(x_bf16: np.ndarray, s):
+    """bf16 bits [R, K] and a calibrated decode scale s -> codes uint8 [R, K]."""
+    x = _c(x_bf16, np.uint16)
+    r, k = x.shape
+    codes = np.empty((r, k), dtype=np.uint8)
+    st = lib().qo_quantize_fp8_static(_ptr(x), r, k, k, float(np.float32(s)), _ptr(codes))
+    if st == 6:
+        raise NonFiniteInput("tensor holds inf or NaN")
+    if st == 1:
+        raise ValueError("scale must be 0 or a normal positive fp32")
+    assert st == 0, st
+    return codes
+
+
+def quantize_nvfp4_static(x_bf16: np.ndarray, s_t):
+    """bf16 bits [R, K] and a calibrated tensor decode scale s_t ->
+    (codes uint8 [R, K/2], block scales uint8 [R, K/16])."""
+    x = _c(x_bf16, np.uint16)
+    r, k = x.shape
+    if k % 16:
+        raise ValueError("NVFP4 needs K % 16 == 0")
+    codes = np.empty((r, k // 2), dtype=np.uint8)
+    bs = np.empty((r, k // 16), dtype=np.uint8)
+    st = lib().qo_quantize_nvfp4_static(_ptr(x), r, k, k, float(np.float32(s_t)), _ptr(codes), _ptr(bs))
+    if st == 6:
+        raise NonFiniteInput("tensor holds inf or NaN")
+    if st == 1:
+        raise ValueError("scale must be 0 or at least 2^-96")
+    assert st == 0, st
+    return codes, bs
+
+
 def linear_reference(kind: str, x_bf16: np.ndarray, w_bf16: np.ndarray, rows=None, cols=None):
     """Oracle for one quantized linear Y = X . W^T.
 

@@ -183,21 +183,56 @@ static int tensor_amax(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld
  *   q = E4M3_RNE_sat(fl(x * r))
  * Output: codes [rows, cols] row-major, and s.
  */
-int qo_quantize_fp8(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
-                    uint8_t *codes, float *scale_out)
+/* The element step of FP8 quantization with a given decode scale s:
+ * r = s > 0 ? fl(1/s) : 0;  q = E4M3_RNE_sat(fl(x * r)). */
+static void quantize_fp8_core(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                              float s, uint8_t *codes)
 {
-    float amax, s, r;
-    int st = tensor_amax(x, rows, cols, ldx, &amax);
-    if (st != QO_OK)
-        return st;
-    s = amax / 448.0f;
-    r = (s > 0.0f) ? 1.0f / s : 0.0f;
+    float r = (s > 0.0f) ? 1.0f / s : 0.0f;
     for (int64_t i = 0; i < rows; ++i)
         for (int64_t c = 0; c < cols; ++c) {
             float y = bf16_to_f32(x[i * ldx + c]) * r;
             codes[i * cols + c] = qo_e4m3_encode(y);
         }
+}
+
+int qo_quantize_fp8(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                    uint8_t *codes, float *scale_out)
+{
+    float amax, s;
+    int st = tensor_amax(x, rows, cols, ldx, &amax);
+    if (st != QO_OK)
+        return st;
+    s = amax / 448.0f;
+    quantize_fp8_core(x, rows, cols, ldx, s, codes);
     *scale_out = s;
+    return QO_OK;
+}
+
+/*
+ * Static (calibrated) scales: the decode scale comes from calibration data
+ * instead of the tensor itself (post-training quantization with fixed
+ * activation ranges). The element step is the one above; values beyond the
+ * calibrated range saturate. The scale must be 0 or a normal positive fp32
+ * (so that 1/s is finite); inputs must be finite.
+ */
+#define QO_ERR_INVALID 1
+static int scale_ok(float s, float min_normal)
+{
+    return s == 0.0f || (isfinite(s) && s >= min_normal);
+}
+
+int qo_quantize_fp8_static(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                           float s, uint8_t *codes)
+{
+    float amax;
+    int st;
+    if (!scale_ok(s, 0x1p-126f))
+        return QO_ERR_INVALID;
+    st = tensor_amax(x, rows, cols, ldx, &amax);  /* finiteness check only */
+    if (st != QO_OK)
+        return st;
+    quantize_fp8_core(x, rows, cols, ldx, s, codes);
     return QO_OK;
 }
 
@@ -220,18 +255,12 @@ int qo_quantize_fp8(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
  * Codes are packed two per byte, element 2i in the low nibble.
  * Outputs: codes [rows, cols/2], block scales [rows, cols/16], s_t.
  */
-int qo_quantize_nvfp4(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
-                      uint8_t *codes, uint8_t *block_scales, float *tscale_out)
+/* The block and element steps of NVFP4 quantization with a given tensor
+ * decode scale s_t (everything after the tensor amax above). */
+static void quantize_nvfp4_core(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                                float s_t, uint8_t *codes, uint8_t *block_scales)
 {
-    float amax, s_t, d_t;
-    int st;
-    if (cols % 16 != 0)
-        return QO_ERR_SHAPE;
-    st = tensor_amax(x, rows, cols, ldx, &amax);
-    if (st != QO_OK)
-        return st;
-    s_t = amax / 2688.0f;
-    d_t = 6.0f * s_t;
+    float d_t = 6.0f * s_t;
     for (int64_t i = 0; i < rows; ++i) {
         for (int64_t b = 0; b < cols / 16; ++b) {
             const uint16_t *xb = x + i * ldx + b * 16;
@@ -254,7 +283,39 @@ int qo_quantize_nvfp4(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx
             }
         }
     }
+}
+
+int qo_quantize_nvfp4(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                      uint8_t *codes, uint8_t *block_scales, float *tscale_out)
+{
+    float amax, s_t;
+    int st;
+    if (cols % 16 != 0)
+        return QO_ERR_SHAPE;
+    st = tensor_amax(x, rows, cols, ldx, &amax);
+    if (st != QO_OK)
+        return st;
+    s_t = amax / 2688.0f;
+    quantize_nvfp4_core(x, rows, cols, ldx, s_t, codes, block_scales);
     *tscale_out = s_t;
+    return QO_OK;
+}
+
+/* Static tensor scale (see qo_quantize_fp8_static): s_t must be 0 or at
+ * least 2^-96, which keeps every effective block scale's reciprocal finite. */
+int qo_quantize_nvfp4_static(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                             float s_t, uint8_t *codes, uint8_t *block_scales)
+{
+    float amax;
+    int st;
+    if (cols % 16 != 0)
+        return QO_ERR_SHAPE;
+    if (!scale_ok(s_t, 0x1p-96f))
+        return QO_ERR_INVALID;
+    st = tensor_amax(x, rows, cols, ldx, &amax);  /* finiteness check only */
+    if (st != QO_OK)
+        return st;
+    quantize_nvfp4_core(x, rows, cols, ldx, s_t, codes, block_scales);
     return QO_OK;
 }
 

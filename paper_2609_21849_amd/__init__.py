@@ -23,7 +23,7 @@ QG_OUT_BF16, QG_OUT_F32 = 0, 1
 QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
                 4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
-EXPORTS = ["qg_quantize_act", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
+EXPORTS = ["qg_quantize_act", "qg_quantize_act_static", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
            "qg_dequant", "qg_status_string", "qg_last_hip_error", "qg_abi_version"]
 
 
@@ -47,6 +47,8 @@ def lib() -> ctypes.CDLL:
         P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
         L.qg_quantize_act.restype = I32
         L.qg_quantize_act.argtypes = [I32, P, I64, I64, I64, P, P, P, P]
+        L.qg_quantize_act_static.restype = I32
+        L.qg_quantize_act_static.argtypes = [I32, P, I64, I64, I64, P, P, P, P]
         L.qg_packed_bytes.restype = SZ
         L.qg_packed_bytes.argtypes = [I32, I64, I64]
         L.qg_pack_weights.restype = I32
@@ -93,6 +95,14 @@ def qg_quantize_act(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale, 
     s = lib().qg_quantize_act(fmt, _p(x), rows, cols, ldx, _p(codes), _p(block_scales), _p(tensor_scale), _stream(stream))
     if check:
         _check(s, "qg_quantize_act")
+    return s
+
+
+def qg_quantize_act_static(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale, stream=None, check=True):
+    s = lib().qg_quantize_act_static(fmt, _p(x), rows, cols, ldx, _p(codes), _p(block_scales), _p(tensor_scale),
+                                     _stream(stream))
+    if check:
+        _check(s, "qg_quantize_act_static")
     return s
 
 
@@ -154,8 +164,10 @@ class QTensor:
     cols: int
 
 
-def quantize(x, fmt: int, stream=None) -> QTensor:
-    """Quantize a [rows, cols] bf16 CUDA tensor (row stride may exceed cols)."""
+def quantize(x, fmt: int, stream=None, static_scale=None) -> QTensor:
+    """Quantize a [rows, cols] bf16 CUDA tensor (row stride may exceed cols).
+    With static_scale (a one-element fp32 CUDA tensor holding a calibrated
+    decode scale) the scale is used as given instead of derived from x."""
     import torch
     assert x.dtype == torch.bfloat16 and x.dim() == 2 and x.stride(1) == 1
     rows, cols = x.shape
@@ -166,8 +178,11 @@ def quantize(x, fmt: int, stream=None) -> QTensor:
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
         bs = torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev)
-    ts = torch.empty(1, dtype=torch.float32, device=dev)
     ldx = x.stride(0) if rows > 1 else cols   # a size-1 dimension may carry any stride
+    if static_scale is not None:
+        qg_quantize_act_static(fmt, x, rows, cols, ldx, codes, bs, static_scale, stream)
+        return QTensor(fmt, codes, bs, static_scale, rows, cols)
+    ts = torch.empty(1, dtype=torch.float32, device=dev)
     qg_quantize_act(fmt, x, rows, cols, ldx, codes, bs, ts, stream)
     return QTensor(fmt, codes, bs, ts, rows, cols)
 

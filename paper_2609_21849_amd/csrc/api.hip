@@ -67,6 +67,25 @@ qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t co
                                         reinterpret_cast<uint8_t*>(block_scales), tensor_scale, st));
 }
 
+qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
+                                 void* codes, void* block_scales, const float* tensor_scale, void* stream) {
+  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
+  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+  if (rows > 0 && cols > 0) {
+    if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+  }
+  return hip_status(qg::launch_quantize_static((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
+                                               reinterpret_cast<uint8_t*>(codes),
+                                               reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                               reinterpret_cast<hipStream_t>(stream)));
+}
+
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k) {
   if (fmt != QG_FMT_FP8_E4M3 && fmt != QG_FMT_NVFP4) return 0;
   if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim || n % 16 != 0 || k % 128 != 0) return 0;
@@ -129,6 +148,14 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
   if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
   if (w_packed_bytes < (size_t)qg::packed_total_bytes((int)w_fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
+  // operands are addressed with 32-bit byte offsets: every operand extent
+  // (activation rows, their block scales, the packed weight) must stay below 2 GiB
+  if (m > 0 && k > 0) {
+    const int64_t esz2 = w8a8 ? 2 : (w4a4 ? 1 : 4);  // element size x 2
+    const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
+    if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
+  }
+  if (qg::packed_total_bytes((int)w_fmt, n, k) > kMaxDim) return QG_ERR_SHAPE;
   if (m > 0 && n > 0) {
     if (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2)) return QG_ERR_INVALID_ARG;
     if (k > 0) {

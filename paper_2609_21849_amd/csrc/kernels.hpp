@@ -30,6 +30,8 @@ inline int64_t packed_total_bytes(int fmt, int64_t n, int64_t k) {
   return kPackHeader + packed_codes_bytes(fmt, n, k) + (fmt == 2 ? padded_rows(n) * k / 16 : 0);
 }
 
+hipError_t launch_quantize_static(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                                  uint8_t* codes, uint8_t* bscale, const float* tscale, hipStream_t st);
 hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
                            uint8_t* codes, uint8_t* bscale, float* tscale, hipStream_t st);
 hipError_t launch_dequant(int fmt, const uint8_t* codes, const uint8_t* bscale, const float* tscale,

@@ -362,6 +362,47 @@ __global__ void __launch_bounds__(256) k_dequant_nvfp4(const uint8_t* __restrict
 // ---------------------------------------------------------------- launchers
 static inline unsigned grid_for(int64_t threads) { return (unsigned)((threads + 255) / 256); }
 
+// The element kernels alone, reading a finished decode scale from `tscale`:
+// the last kernel of the dynamic chain, and the whole of a quantization with
+// a static (calibrated) scale.
+hipError_t launch_quantize_static(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                                  uint8_t* codes, uint8_t* bscale, const float* tscale, hipStream_t st) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const bool contig = (ldx == cols);
+  const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0);
+  const int64_t n = rows * cols;
+  const bool qal = (reinterpret_cast<uintptr_t>(codes) % 8 == 0);
+  if (contig && aligned && qal) {
+    const unsigned g = (unsigned)((n + 8191) / 8192);  // 4 waves x 2048 elements per workgroup
+    if (fmt == 1) hipLaunchKernelGGL((k_quant_dense<1, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+    else hipLaunchKernelGGL((k_quant_dense<2, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
+  } else if (fmt == 1) {
+    const bool qal16 = (reinterpret_cast<uintptr_t>(codes) % 16 == 0);
+    if (contig) {
+      const bool vec = aligned && qal16;
+      const unsigned g = grid_for((rows * cols + 15) / 16);
+      if (vec) hipLaunchKernelGGL((k_quant_fp8<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
+      else hipLaunchKernelGGL((k_quant_fp8<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
+    } else {
+      const bool vec = aligned && qal16 && (ldx % 8 == 0) && (cols % 16 == 0);
+      const unsigned g = grid_for(rows * ((cols + 15) / 16));
+      if (vec) hipLaunchKernelGGL((k_quant_fp8<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
+      else hipLaunchKernelGGL((k_quant_fp8<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
+    }
+  } else {
+    const unsigned g = grid_for(rows * (cols / 16));
+    const bool vec = aligned && (contig || ldx % 8 == 0);
+    if (contig) {
+      if (vec) hipLaunchKernelGGL((k_quant_nvfp4<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
+      else hipLaunchKernelGGL((k_quant_nvfp4<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
+    } else {
+      if (vec) hipLaunchKernelGGL((k_quant_nvfp4<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
+      else hipLaunchKernelGGL((k_quant_nvfp4<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
+    }
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
                            uint8_t* codes, uint8_t* bscale, float* tscale, hipStream_t st) {
   if (rows == 0 || cols == 0) {
@@ -404,37 +445,7 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
     hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, st, partial, (int)(gx * gy), tscale,
                        fmt == 1 ? 448.0f : 2688.0f);
   }
-  const int64_t n = rows * cols;
-  const bool qal = (reinterpret_cast<uintptr_t>(codes) % 8 == 0);
-  if (contig && aligned && qal) {
-    const unsigned g = (unsigned)((n + 8191) / 8192);  // 4 waves x 2048 elements per workgroup
-    if (fmt == 1) hipLaunchKernelGGL((k_quant_dense<1, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
-    else hipLaunchKernelGGL((k_quant_dense<2, 4>), dim3(g), dim3(256), 0, st, x, n, codes, bscale, tscale);
-  } else if (fmt == 1) {
-    const bool qal16 = (reinterpret_cast<uintptr_t>(codes) % 16 == 0);
-    if (contig) {
-      const bool vec = aligned && qal16;
-      const unsigned g = grid_for((rows * cols + 15) / 16);
-      if (vec) hipLaunchKernelGGL((k_quant_fp8<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
-      else hipLaunchKernelGGL((k_quant_fp8<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
-    } else {
-      const bool vec = aligned && qal16 && (ldx % 8 == 0) && (cols % 16 == 0);
-      const unsigned g = grid_for(rows * ((cols + 15) / 16));
-      if (vec) hipLaunchKernelGGL((k_quant_fp8<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
-      else hipLaunchKernelGGL((k_quant_fp8<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, tscale);
-    }
-  } else {
-    const unsigned g = grid_for(rows * (cols / 16));
-    const bool vec = aligned && (contig || ldx % 8 == 0);
-    if (contig) {
-      if (vec) hipLaunchKernelGGL((k_quant_nvfp4<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
-      else hipLaunchKernelGGL((k_quant_nvfp4<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
-    } else {
-      if (vec) hipLaunchKernelGGL((k_quant_nvfp4<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
-      else hipLaunchKernelGGL((k_quant_nvfp4<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, bscale, tscale);
-    }
-  }
-  return hipGetLastError();
+  return launch_quantize_static(fmt, x, rows, cols, ldx, codes, bscale, tscale, st);
 }
 
 hipError_t launch_dequant(int fmt, const uint8_t* codes, const uint8_t* bscale, const float* tscale,

@@ -73,6 +73,23 @@ def test_quantize_validation():
     assert _quant(FP8, bs=None, ts=P + 2) == INVALID
 
 
+def _quant_static(fmt, x=P, rows=4, cols=32, ldx=32, codes=P, bs=P, ts=P):
+    return q.qg_quantize_act_static(fmt, x, rows, cols, ldx, codes, bs, ts, stream=0, check=False)
+
+
+def test_static_quantize_validation():
+    assert _quant_static(9) == INVALID
+    assert _quant_static(BF16) == UNSUP
+    assert _quant_static(NVFP4, cols=24, ldx=24) == SHAPE
+    assert _quant_static(NVFP4, ts=None) == INVALID
+    assert _quant_static(NVFP4, x=None) == INVALID
+    assert _quant_static(NVFP4, bs=None) == INVALID
+    assert _quant_static(NVFP4, codes=P + 4) == INVALID
+    assert _quant_static(NVFP4, ldx=16) == INVALID
+    assert _quant_static(FP8, bs=P) == INVALID
+    assert _quant_static(FP8, bs=None, ts=P + 2) == INVALID
+
+
 def _pack(fmt, codes=P, bs=P, ts=P, n=32, k=128, packed=P, nbytes=1 << 20, unpack=False):
     if unpack:
         return q.qg_unpack_weights(fmt, packed, nbytes, n, k, codes, bs, ts, stream=0, check=False)
@@ -118,6 +135,9 @@ def test_gemm_validation():
     assert _gemm(abs_=None) == INVALID                                   # W4A4 needs A block scales
     assert _gemm(lda=512) == INVALID                                     # W4A4 codes are dense
     assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, a=P + 8) == INVALID     # 16-byte alignment
+    # operand extents above 2 GiB (32-bit buffer offsets)
+    assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, m=70000, lda=32768, k=32768) == SHAPE
+    assert _gemm(a_fmt=BF16, abs_=None, ats=None, m=40000, lda=32768, k=32768) == SHAPE
     assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, ats=None) == INVALID
     assert _gemm(a_fmt=FP8, w_fmt=FP8) == INVALID                         # FP8 A has no block scales
     assert _gemm(a_fmt=BF16, abs_=None, ats=P) == INVALID                 # bf16 A has no scales

@@ -207,3 +207,34 @@ def test_w4a16_weight_pool_sampled(m, k):
     rows, cols = _sample(m, n, 2000, 3)
     ref = oracle.linear_reference("w4a16", x, w, rows=rows, cols=cols)
     log("  max err/B", check_linear(y, ref, rows, cols))
+
+
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4"])
+def test_linear_with_calibrated_activation_scale(kind):
+    # static activation scale calibrated on other batches (the max of their
+    # dynamic scales), applied to a new batch: quantize once with the given
+    # scale, then the GEMM; reference = oracle static codes x oracle weights
+    m, n, k = 300, 272, 384
+    fmt = q.QG_FMT_FP8_E4M3 if kind == "fp8" else q.QG_FMT_NVFP4
+    cal = [synth.normal_bf16(m, k, 1.0, 20 + i, 0) for i in range(3)]
+    x = synth.normal_bf16(m, k, 1.3, 30, 0)          # wider than the calibration data: some saturation
+    w = synth.normal_bf16(n, k, 0.02, 30, 1)
+    if kind == "fp8":
+        s = max(oracle.quantize_fp8(c)[1] for c in cal)
+        qa = oracle.quantize_fp8_static(x, s)
+        a_ref = oracle.dequant_fp8(qa, s)
+        qw, sw = oracle.quantize_fp8(w)
+        w_ref = oracle.dequant_fp8(qw, sw)
+    else:
+        s = max(oracle.quantize_nvfp4(c)[2] for c in cal)
+        qa, ba = oracle.quantize_nvfp4_static(x, s)
+        a_ref = oracle.dequant_nvfp4(qa, ba, s)
+        qw, bw, sw = oracle.quantize_nvfp4(w)
+        w_ref = oracle.dequant_nvfp4(qw, bw, sw)
+    y_ref, b = oracle.gemm_f64(a_ref, w_ref)
+    sd = torch.tensor([np.float32(s)], dtype=torch.float32, device=DEV)
+    a = q.quantize(to_dev_bf16(x), fmt, static_scale=sd)
+    packed = q.pack(q.quantize(to_dev_bf16(w), fmt))
+    y = q.linear(a, packed, fmt, n, out_dtype=q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    log("  static %s max err/B" % kind, check_linear(y, {"y": y_ref, "b": b}))

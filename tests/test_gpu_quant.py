@@ -156,3 +156,50 @@ def test_pack_unpack_roundtrip(fmt, n, k):
     body = host(packed)[256:256 + codes.size + pad_rows * codes.shape[1]]
     expect = np.concatenate([codes.reshape(-1), np.zeros(pad_rows * codes.shape[1], np.uint8)])
     assert np.array_equal(np.sort(body), np.sort(expect))
+
+
+# ---------------------------------------------------------------- static (calibrated) scales
+STATIC_SHAPES = [(1, 16), (37, 160), (512, 3072), (4608, 3072), (257, 400)]
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("rows,cols", STATIC_SHAPES)
+@pytest.mark.parametrize("factor", [1.0, 0.5, 0.3, 3.0, 0.0])
+def test_static_quantize_bit_exact(fmt, rows, cols, factor):
+    # the calibrated scale: the tensor's own dynamic scale (codes must equal
+    # the dynamic codes), smaller ones (saturation beyond the calibrated
+    # range), a larger one and zero
+    log("static quantize fmt=%d shape=%dx%d factor=%g" % (fmt, rows, cols, factor))
+    x = synth.normal_bf16(rows, cols, 1.0, 7, 0, outlier_frac=0.001, outlier_gain=50.0)
+    if fmt == FP8:
+        _, s_dyn = oracle.quantize_fp8(x)
+    else:
+        _, _, s_dyn = oracle.quantize_nvfp4(x)
+    s = np.float32(s_dyn * np.float32(factor))
+    sd = torch.tensor([s], dtype=torch.float32, device=DEV)
+    qt = q.quantize(to_dev_bf16(x), fmt, static_scale=sd)
+    torch.cuda.synchronize()
+    assert scale_of(sd).view(np.uint32) == s.view(np.uint32)      # the scale is an input only
+    if fmt == FP8:
+        ref = oracle.quantize_fp8_static(x, s)
+        nbad = int(np.count_nonzero(host(qt.codes) != ref))
+        assert nbad == 0, "fp8 static codes differ at %d of %d" % (nbad, ref.size)
+    else:
+        rc, rb = oracle.quantize_nvfp4_static(x, s)
+        assert int(np.count_nonzero(host(qt.codes) != rc)) == 0
+        assert int(np.count_nonzero(host(qt.block_scales) != rb)) == 0
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_static_quantize_strided_rows(fmt):
+    full = synth.normal_bf16(64, 400, 1.0, 8, 0)
+    xd = to_dev_bf16(full)[:, :320]
+    x = np.ascontiguousarray(full[:, :320])
+    s = np.float32(0.004)
+    qt = q.quantize(xd, fmt, static_scale=torch.tensor([s], device=DEV))
+    torch.cuda.synchronize()
+    if fmt == FP8:
+        assert np.array_equal(host(qt.codes), oracle.quantize_fp8_static(x, s))
+    else:
+        rc, rb = oracle.quantize_nvfp4_static(x, s)
+        assert np.array_equal(host(qt.codes), rc) and np.array_equal(host(qt.block_scales), rb)

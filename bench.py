@@ -223,16 +223,17 @@ def main():
                 bs = torch.empty((M, k // 16), dtype=torch.uint8, device="cuda")
             ent["a_" + kind] = q.QTensor(fmt, codes, bs, torch.empty(1, device="cuda"), M, k)
             ent["y_" + kind] = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
+        ent["w_bf16"] = wd  # for the BF16 baseline of the block chain
         dit.append(ent)
-        del wd
     enc = []
     for ei, (name, (n, k)) in enumerate(synth.ENCODER_LINEARS.items()):
         base = 64 + 16 * ei
         w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
         packed = q.pack(q.quantize(dev_bf16(w), q.QG_FMT_NVFP4))
+        packed8 = q.pack(q.quantize(dev_bf16(w), q.QG_FMT_FP8_E4M3))
         for m in synth.ENCODER_TOKENS:
             x = dev_bf16(synth.normal_bf16(m, k, synth.SIGMA_X, 0, base + synth.STREAM_X + 100 * m))
-            enc.append({"name": name, "n": n, "k": k, "m": m, "x": x, "w": packed,
+            enc.append({"name": name, "n": n, "k": k, "m": m, "x": x, "w": packed, "w8": packed8,
                         "y": torch.empty((m, n), dtype=torch.bfloat16, device="cuda")})
     torch.cuda.synchronize()
     t_setup = time.time() - t_setup
@@ -329,6 +330,8 @@ def main():
     parts["w4a16_single_call"] = w4
     parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
     parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
+    parts["dit_block_chain"] = block_chain_part(q, dit, M)
+    parts["w8a8_encoder"] = w8a8_encoder_part(q, enc)
     parts["w4a16_cold_pool"] = w4a16_pool(q, synth, args.pool_mib)
 
     # dominant kernel: the GEMM kind with the largest share of the step
@@ -368,6 +371,93 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def w8a8_encoder_part(q, enc, reps=20):
+    """W8A8 at the text-encoder shapes (the FP8 alternative to W4A16 for the
+    small encoder): dynamic activation quantize + FP8 GEMM per call, with
+    preallocated buffers and raw C-ABI launches (HIP events per launch)."""
+    import torch
+    lib = q.lib()
+    st = torch.cuda.current_stream().cuda_stream
+    out = {}
+    for e in enc:
+        m, n, k = e["m"], e["n"], e["k"]
+        codes = torch.empty((m, k), dtype=torch.uint8, device="cuda")
+        ts = torch.empty(1, dtype=torch.float32, device="cuda")
+        y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+        qargs = (q.QG_FMT_FP8_E4M3, e["x"].data_ptr(), m, k, k, codes.data_ptr(), None, ts.data_ptr(), st)
+        gargs = (q.QG_FMT_FP8_E4M3, codes.data_ptr(), None, ts.data_ptr(), k, q.QG_FMT_FP8_E4M3,
+                 e["w8"].data_ptr(), e["w8"].numel(), m, n, k, y.data_ptr(), n, q.QG_OUT_BF16, st)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps + 3)]
+        for i in range(reps + 3):
+            evs[i][0].record()
+            assert lib.qg_quantize_act(*qargs) == 0
+            evs[i][1].record()
+            assert lib.qg_gemm(*gargs) == 0
+            evs[i][2].record()
+        torch.cuda.synchronize()
+        qus = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in evs[3:]])) * 1e3
+        gus = float(np.mean([ev[1].elapsed_time(ev[2]) for ev in evs[3:]])) * 1e3
+        out["%s_m%d" % (e["name"], m)] = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2),
+                                            "gemm_tflops": round(2 * m * n * k / (gus * 1e6), 2)}
+    return out
+
+
+def block_chain_part(q, dit, M, steps=10):
+    """The four linears of one transformer block as a chain, data flowing
+    through: QKV -> (attention stubbed: the V third of the QKV output) ->
+    attention-out -> MLP-up -> GELU -> MLP-down, in BF16 (hipBLASLt through
+    torch.mm: the unquantized baseline), FP8 W8A8 and NVFP4 W4A4 (this
+    library: dynamic activation quantization + GEMM per linear). Same
+    weights, same input; GELU and the slice are shared glue. Reports the
+    chain time per precision and the speed-up over BF16 (the paper's step
+    ratio of BF16 -> FP8 -> NVFP4 comes from these linears)."""
+    import torch
+    import torch.nn.functional as F
+    by = {e["name"]: e for e in dit}
+    x0 = dit[0]["x"]["fp8"]  # N(0,1) input of the block [M, 3072]
+
+    def chain_bf16():
+        h = torch.mm(x0, by["qkv"]["w_bf16"].t())
+        v = h[:, 6144:9216]
+        a = torch.mm(v, by["attn_out"]["w_bf16"].t())
+        u = F.gelu(torch.mm(a, by["mlp_up"]["w_bf16"].t()), approximate="tanh")
+        return torch.mm(u, by["mlp_down"]["w_bf16"].t())
+
+    def chain_q(kind, fmt):
+        def lin(x, name):
+            e = by[name]
+            return q.linear(q.quantize(x, fmt), e["w_" + kind], fmt, e["n"])
+        h = lin(x0, "qkv")
+        v = h[:, 6144:9216]
+        a = lin(v, "attn_out")
+        u = F.gelu(lin(a, "mlp_up"), approximate="tanh")
+        return lin(u, "mlp_down")
+
+    runs = {"bf16": chain_bf16, "fp8": lambda: chain_q("fp8", q.QG_FMT_FP8_E4M3),
+            "nvfp4": lambda: chain_q("nvfp4", q.QG_FMT_NVFP4)}
+    res = {}
+    outs = {}
+    for name, fn in runs.items():
+        for _ in range(2):
+            outs[name] = fn()
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(steps):
+            fn()
+        s1.record()
+        torch.cuda.synchronize()
+        res[name] = {"ms": round(s0.elapsed_time(s1) / steps, 4)}
+    for name in ("fp8", "nvfp4"):
+        res[name]["speedup_vs_bf16"] = round(res["bf16"]["ms"] / res[name]["ms"], 3)
+        # agreement of the chain output with the BF16 chain (relative Frobenius error)
+        d = (outs[name].float() - outs["bf16"].float()).norm() / outs["bf16"].float().norm()
+        res[name]["rel_err_vs_bf16"] = round(float(d), 4)
+    res["note"] = ("chain time includes the activation quantizers, GELU and the allocating Python "
+                   "helpers; attention is stubbed")
+    return res
 
 
 def static_scale_part(q, lib, st, dit, M, flops, steps=10):

@@ -59,6 +59,14 @@ def lib() -> ctypes.CDLL:
         L.qo_quantize_fp8.argtypes = [P, I64, I64, I64, P, P]
         L.qo_quantize_nvfp4.restype = ctypes.c_int
         L.qo_quantize_nvfp4.argtypes = [P, I64, I64, I64, P, P, P]
+        L.qo_e8m0_value.restype = ctypes.c_double
+        L.qo_e8m0_value.argtypes = [ctypes.c_uint8]
+        L.qo_quantize_mxfp4.restype = ctypes.c_int
+        L.qo_quantize_mxfp4.argtypes = [P, I64, I64, I64, P, P]
+        L.qo_quantize_mxfp8.restype = ctypes.c_int
+        L.qo_quantize_mxfp8.argtypes = [P, I64, I64, I64, P, P]
+        L.qo_dequant_mxfp4_f64.argtypes = [P, P, I64, I64, P]
+        L.qo_dequant_mxfp8_f64.argtypes = [P, P, I64, I64, P]
         L.qo_quantize_fp8_static.restype = ctypes.c_int
         L.qo_quantize_fp8_static.argtypes = [P, I64, I64, I64, ctypes.c_float, P]
         L.qo_quantize_nvfp4_static.restype = ctypes.c_int
@@ -272,12 +280,48 @@ def quantize_nvfp4_static(x_bf16: np.ndarray, s_t):
     return codes, bs
 
 
+def e8m0_table():
+    """Values of the 255 finite E8M0 scale codes (code 255 is NaN)."""
+    return np.array([lib().qo_e8m0_value(c) for c in range(256)])
+
+
+def quantize_mx(x_bf16: np.ndarray, fmt: str):
+    """bf16 bits [R, K] -> (codes, E8M0 scales uint8 [R, K/32]) for fmt in
+    {"mxfp4", "mxfp8"} (OCP MX, blocks of 32 along K, no tensor scale)."""
+    x = _c(x_bf16, np.uint16)
+    r, k = x.shape
+    if k % 32:
+        raise ValueError("MX formats need K % 32 == 0")
+    codes = np.zeros((r, k // 2) if fmt == "mxfp4" else (r, k), dtype=np.uint8)
+    sc = np.empty((r, k // 32), dtype=np.uint8)
+    fn = lib().qo_quantize_mxfp4 if fmt == "mxfp4" else lib().qo_quantize_mxfp8
+    st = fn(_ptr(x), r, k, k, _ptr(codes), _ptr(sc))
+    if st == 6:
+        raise NonFiniteInput("tensor holds inf or NaN")
+    assert st == 0, st
+    return codes, sc
+
+
+def dequant_mx(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.ndarray:
+    """Exact (binary64) values of MX codes."""
+    c = _c(codes, np.uint8)
+    s = _c(scales, np.uint8)
+    rows = c.shape[0]
+    k = c.shape[1] * 2 if fmt == "mxfp4" else c.shape[1]
+    y = np.empty((rows, k), dtype=np.float64)
+    fn = lib().qo_dequant_mxfp4_f64 if fmt == "mxfp4" else lib().qo_dequant_mxfp8_f64
+    fn(_ptr(c), _ptr(s), rows, k, _ptr(y))
+    return y
+
+
 def linear_reference(kind: str, x_bf16: np.ndarray, w_bf16: np.ndarray, rows=None, cols=None):
     """Oracle for one quantized linear Y = X . W^T.
 
     kind = "fp8"   : both operands FP8 E4M3, per-tensor scales (W8A8)
            "nvfp4" : both operands NVFP4 (W4A4)
            "w4a16" : X stays bf16, W is NVFP4
+           "mxfp4" / "mxfp8": both operands in the OCP MX format (E2M1 / E4M3
+                     elements, E8M0 scale per 32, no tensor scale)
     Returns dict with quantized operands, y (fp64) and b = sum|a w| for the
     full product, or for the (rows[s], cols[s]) samples when given.
     """
@@ -298,6 +342,12 @@ def linear_reference(kind: str, x_bf16: np.ndarray, w_bf16: np.ndarray, rows=Non
             deq_a = lambda idx: dequant_nvfp4(qa[idx], ba[idx], sa)
         else:
             deq_a = lambda idx: bf16_to_f64(x_bf16[idx])
+    elif kind in ("mxfp4", "mxfp8"):
+        qa, sa = quantize_mx(x_bf16, kind)
+        qw, sw = quantize_mx(w_bf16, kind)
+        out.update(a_codes=qa, a_bscales=sa, w_codes=qw, w_bscales=sw)
+        deq_a = lambda idx: dequant_mx(qa[idx], sa[idx], kind)
+        deq_w = lambda idx: dequant_mx(qw[idx], sw[idx], kind)
     else:
         raise ValueError(kind)
     if rows is None:

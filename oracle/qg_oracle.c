@@ -320,6 +320,122 @@ int qo_quantize_nvfp4_static(const uint16_t *x, int64_t rows, int64_t cols, int6
 }
 
 /* ------------------------------------------------------------------ */
+/* MX formats (OCP Microscaling v1.0): the matrix-core-native block    */
+/* scaling of gfx950, a variant beside the paper's NVFP4               */
+/* ------------------------------------------------------------------ */
+/*
+ * Blocks of 32 consecutive elements along a row share one E8M0 scale (an
+ * 8-bit power-of-two exponent, bias 127: value 2^(e - 127); 255 = NaN is
+ * never produced); there is no tensor scale. Per the OCP Microscaling
+ * Formats specification, section on conversion:
+ *   a_b = max |x| over the block
+ *   shared exponent E = floor(log2(a_b)) - emax_elem, where emax_elem is the
+ *     exponent of the element format's largest normal number: 2 for E2M1
+ *     (6 = 1.5 * 2^2), 8 for E4M3 (448 = 1.75 * 2^8)
+ *   e = E + 127 clamped to [0, 254] (e = 0 for an all-zero block)
+ *   q_k = element_RNE_sat(x_k / 2^(e - 127))
+ * Readings where the specification leaves a choice: values above the
+ * element format's largest normal saturate to it (E2M1 has no inf/NaN;
+ * for E4M3 the same saturation as the FP8 recipe), ties round to the even
+ * code, an all-zero block gets e = 0. Division by the power of two is exact
+ * (bf16 inputs keep x / 2^(e-127) inside the binary32 normal range).
+ * Outputs: codes (MXFP4: two per byte, element 2i in the low nibble;
+ * MXFP8: one E4M3 byte per element) and E8M0 scales [rows, cols/32].
+ */
+double qo_e8m0_value(uint8_t e)
+{
+    if (e == 255)
+        return NAN;
+    return ldexp(1.0, (int)e - 127);
+}
+
+static uint8_t mx_scale_code(float a_b, int emax_elem)
+{
+    int ex, e;
+    if (a_b == 0.0f)
+        return 0;
+    frexpf(a_b, &ex);          /* a_b = f * 2^ex, f in [0.5, 1): floor(log2 a_b) = ex - 1 */
+    e = (ex - 1) - emax_elem + 127;
+    if (e < 0)
+        e = 0;
+    if (e > 254)
+        e = 254;
+    return (uint8_t)e;
+}
+
+static int quantize_mx(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                       int fp4, uint8_t *codes, uint8_t *scales)
+{
+    float amax;
+    int st;
+    if (cols % 32 != 0)
+        return QO_ERR_SHAPE;
+    st = tensor_amax(x, rows, cols, ldx, &amax);  /* finiteness check only */
+    if (st != QO_OK)
+        return st;
+    for (int64_t i = 0; i < rows; ++i) {
+        for (int64_t b = 0; b < cols / 32; ++b) {
+            const uint16_t *xb = x + i * ldx + b * 32;
+            float a_b = 0.0f;
+            uint8_t e;
+            for (int t = 0; t < 32; ++t) {
+                float v = fabsf(bf16_to_f32(xb[t]));
+                if (v > a_b)
+                    a_b = v;
+            }
+            e = mx_scale_code(a_b, fp4 ? 2 : 8);
+            scales[i * (cols / 32) + b] = e;
+            for (int t = 0; t < 32; ++t) {
+                float y = ldexpf(bf16_to_f32(xb[t]), 127 - (int)e);
+                if (fp4) {
+                    uint8_t q = qo_e2m1_encode(y);
+                    uint8_t *dst = &codes[i * (cols / 2) + b * 16 + t / 2];
+                    if (t & 1)
+                        *dst = (uint8_t)((*dst & 0x0F) | (q << 4));
+                    else
+                        *dst = q;
+                } else {
+                    codes[i * cols + b * 32 + t] = qo_e4m3_encode(y);
+                }
+            }
+        }
+    }
+    return QO_OK;
+}
+
+int qo_quantize_mxfp4(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                      uint8_t *codes, uint8_t *scales)
+{
+    return quantize_mx(x, rows, cols, ldx, 1, codes, scales);
+}
+
+int qo_quantize_mxfp8(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                      uint8_t *codes, uint8_t *scales)
+{
+    return quantize_mx(x, rows, cols, ldx, 0, codes, scales);
+}
+
+/* Exact values (binary64): x = element(q) * 2^(e - 127). */
+void qo_dequant_mxfp4_f64(const uint8_t *codes, const uint8_t *scales, int64_t rows, int64_t cols,
+                          double *out)
+{
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t c = 0; c < cols; ++c) {
+            uint8_t byte = codes[i * (cols / 2) + c / 2];
+            uint8_t q = (c & 1) ? (byte >> 4) : (byte & 15);
+            out[i * cols + c] = qo_e2m1_value(q) * qo_e8m0_value(scales[i * (cols / 32) + c / 32]);
+        }
+}
+
+void qo_dequant_mxfp8_f64(const uint8_t *codes, const uint8_t *scales, int64_t rows, int64_t cols,
+                          double *out)
+{
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t c = 0; c < cols; ++c)
+            out[i * cols + c] = qo_e4m3_value(codes[i * cols + c]) * qo_e8m0_value(scales[i * (cols / 32) + c / 32]);
+}
+
+/* ------------------------------------------------------------------ */
 /* Dequantization                                                     */
 /* ------------------------------------------------------------------ */
 /* Exact values (binary64): FP8 x = dec(q) * s. */

@@ -12,7 +12,19 @@
  *          16 consecutive elements along a row, one E4M3 scale per block and
  *          one fp32 decode scale per tensor:  x ~ e2m1(q) * e4m3(s_b) * s_t.
  *
- * and a weight-only variant (bf16 activations times NVFP4 weights).
+ * and a weight-only variant (bf16 activations times NVFP4 weights). Beside
+ * them, the OCP Microscaling (MX v1.0) 4- and 8-bit formats, the block
+ * scaling gfx950's matrix cores apply in hardware:
+ *
+ *   MXFP4: E2M1 codes in blocks of 32 consecutive elements along a row, one
+ *          E8M0 scale (a power of two 2^(e-127), e in 0..254) per block and
+ *          no tensor scale:                x ~ e2m1(q) * 2^(e-127).
+ *   MXFP8: the same with E4M3 codes.
+ *
+ * MX is the hardware-native variant of the paper's 4-bit recipe (Sec. 4,
+ * quantization paragraph: activation quantization onto 4-bit matrix units);
+ * its numerics differ from NVFP4's (power-of-two scales per 32 instead of
+ * E4M3 scales per 16), so it is a separate format, not an NVFP4 kernel.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -28,6 +40,8 @@
  *  - NVFP4 codes: two per byte, dense [rows, cols/2]; element 2i of a row
  *    sits in the low nibble of byte i. Block scales: E4M3 bytes, dense
  *    [rows, cols/16]; block j covers elements 16j .. 16j+15 of its row.
+ *  - MX codes: MXFP4 like NVFP4 codes, MXFP8 like FP8 codes. Block scales:
+ *    E8M0 bytes, dense [rows, cols/32]; block j covers elements 32j .. 32j+31.
  *  - Tensor scales are single fp32 values in device memory (decode scales).
  *  - All work is enqueued on `stream` (a hipStream_t; NULL = the default
  *    stream) with no host synchronisation. Argument and shape checks run on
@@ -63,7 +77,9 @@ typedef enum qg_status {
 typedef enum qg_format {
     QG_FMT_BF16 = 0,             /* unquantized bfloat16 */
     QG_FMT_FP8_E4M3 = 1,         /* E4M3 codes + per-tensor fp32 scale */
-    QG_FMT_NVFP4 = 2             /* E2M1 codes + E4M3 per-16 block scales + fp32 tensor scale */
+    QG_FMT_NVFP4 = 2,            /* E2M1 codes + E4M3 per-16 block scales + fp32 tensor scale */
+    QG_FMT_MXFP4 = 3,            /* E2M1 codes + E8M0 per-32 block scales, no tensor scale */
+    QG_FMT_MXFP8 = 4             /* E4M3 codes + E8M0 per-32 block scales, no tensor scale */
 } qg_format;
 
 typedef enum qg_out_dtype {
@@ -77,11 +93,13 @@ typedef enum qg_out_dtype {
  * Paper: Sec. 4, quantization paragraph (activation quantization is what
  * lets the linears run on low-precision units; PTQ of weights).
  *
- *   fmt           QG_FMT_FP8_E4M3 or QG_FMT_NVFP4.
+ *   fmt           QG_FMT_FP8_E4M3, QG_FMT_NVFP4, QG_FMT_MXFP4 or QG_FMT_MXFP8.
  *   x             bf16 [rows, ldx], the first `cols` of each row are used.
- *   codes         out: FP8 [rows, cols] bytes; NVFP4 [rows, cols/2] bytes.
- *   block_scales  out: NVFP4 [rows, cols/16] E4M3 bytes; must be NULL for FP8.
- *   tensor_scale  out: one fp32 decode scale.
+ *   codes         out: FP8/MXFP8 [rows, cols] bytes; NVFP4/MXFP4 [rows, cols/2]
+ *                 bytes (MXFP4: 4-byte aligned).
+ *   block_scales  out: NVFP4 [rows, cols/16] E4M3 bytes; MX [rows, cols/32]
+ *                 E8M0 bytes; must be NULL for FP8.
+ *   tensor_scale  out: one fp32 decode scale; must be NULL for the MX formats.
  *   The tensor-wide max is reduced in two kernels whose partial results are
  *   parked in `codes` (overwritten by the codes afterwards) or, for tensors
  *   of a few elements, in `tensor_scale`; so x, codes, block_scales and
@@ -92,10 +110,15 @@ typedef enum qg_out_dtype {
  *   NVFP4: a = max|x|; s_t = a/2688; d = 6*s_t; per block b:
  *          v = d>0 ? max_b|x|/d : 0; s_b = E4M3(v); S = e4m3(s_b)*s_t;
  *          r = S>0 ? 1/S : 0; q = E2M1(x*r)
+ *   MX   : per block b: a_b = max_b|x|; e = a_b > 0 ? clamp(floor(log2 a_b)
+ *          - emax + 127, 0, 254) : 0 (emax = 2 for E2M1, 8 for E4M3);
+ *          q = E2M1 / E4M3(x * 2^(127-e)) (the product is exact). OCP MX
+ *          v1.0, scale and element conversion; one kernel, no reduction
+ *          across the tensor.
  *   E4M3()/E2M1() round to nearest, ties to the even code, saturate at
  *   +-448 / +-6, and keep the sign of zero.
- * Shapes: rows, cols >= 0; NVFP4 needs cols % 16 == 0 (QG_ERR_SHAPE).
- * An empty tensor gets tensor_scale = 0.
+ * Shapes: rows, cols >= 0; NVFP4 needs cols % 16 == 0, MX cols % 32 == 0
+ * (QG_ERR_SHAPE). An empty tensor gets tensor_scale = 0 (none for MX).
  */
 qg_status qg_quantize_act(qg_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
                           void *codes, void *block_scales, float *tensor_scale, void *stream);
@@ -117,15 +140,16 @@ qg_status qg_quantize_act(qg_format fmt, const void *x, int64_t rows, int64_t co
  * with the given scale; elements beyond the calibrated range saturate to
  * +-448 (FP8) or to a block scale of 448 and codes of +-6 (NVFP4). With the
  * scale qg_quantize_act would derive, the codes are identical to its codes.
- * An empty tensor enqueues nothing.
+ * An empty tensor enqueues nothing. The MX formats have no tensor scale:
+ * QG_ERR_UNSUPPORTED.
  */
 qg_status qg_quantize_act_static(qg_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
                                  void *codes, void *block_scales, const float *tensor_scale, void *stream);
 
 /*
  * qg_packed_bytes -- size of the packed weight buffer for an [n, k] weight
- * in `fmt` (FP8 or NVFP4), or 0 when the shape breaks the GEMM contract
- * (n % 16, k % 128) or the format is not packable.
+ * in `fmt` (FP8, NVFP4 or MXFP4), or 0 when the shape breaks the GEMM
+ * contract (n % 16, k % 128; MXFP4 k % 256) or the format is not packable.
  */
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
 
@@ -137,10 +161,11 @@ size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
  * like the cached engines of Sec. 5).
  *
  *   codes, block_scales, tensor_scale: as written by qg_quantize_act
- *                 (block_scales NULL for FP8).
+ *                 (block_scales NULL for FP8; tensor_scale NULL for MXFP4).
  *   packed        out: qg_packed_bytes(fmt, n, k) bytes, 256-byte aligned.
  * The layout is private to this library version (qg_unpack_weights is its
- * exact inverse). Shapes: n % 16 == 0 and k % 128 == 0, else QG_ERR_SHAPE.
+ * exact inverse). Shapes: n % 16 == 0 and k % 128 == 0 (MXFP4: k % 256),
+ * else QG_ERR_SHAPE. MXFP8 weights are not packable: QG_ERR_UNSUPPORTED.
  */
 qg_status qg_pack_weights(qg_format fmt, const void *codes, const void *block_scales,
                           const float *tensor_scale, int64_t n, int64_t k,
@@ -164,12 +189,16 @@ qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_byt
  *   (FP8_E4M3, FP8_E4M3)  W8A8:  a = codes [m, k] (lda = k), a_block_scales NULL
  *   (NVFP4,    NVFP4)     W4A4:  a = codes [m, k/2], a_block_scales [m, k/16] (lda = k)
  *   (BF16,     NVFP4)     W4A16: a = bf16 [m, lda], a_block_scales and a_tensor_scale NULL
- *   a_tensor_scale  device fp32 decode scale of A (quantized formats).
+ *   (MXFP4,    MXFP4)     MX W4A4: a = codes [m, k/2], a_block_scales [m, k/32]
+ *                         (8-byte aligned, lda = k), a_tensor_scale NULL;
+ *                         k % 256 == 0. The E8M0 block scales of both
+ *                         operands are applied by the matrix instruction.
+ *   a_tensor_scale  device fp32 decode scale of A (FP8, NVFP4).
  *   w_packed        buffer written by qg_pack_weights for an [n, k] weight.
  *   y               out: [m, ldy] of y_dtype.
  * Result: y[i,j] = s_a * s_w * sum_k deq'(a)[i,k] deq'(w)[j,k] with fp32
  * accumulation (deq' = decoded codes times block scales; the tensor scales
- * are applied once at the end), then rounded to y_dtype. Accuracy contract:
+ * are applied once at the end; MX has none), then rounded to y_dtype. Accuracy contract:
  * |y - y_exact| <= 1e-3 * sum_k |a w| plus the rounding of y to y_dtype.
  * Shapes: m, n, k >= 0; n % 16 == 0; k % 128 == 0; lda >= k, ldy >= n.
  * Operands are addressed with 32-bit byte offsets: the activation extent
@@ -186,8 +215,11 @@ qg_status qg_gemm(qg_format a_fmt, const void *a, const void *a_block_scales,
  * qg_dequant -- decode a quantized tensor to bf16 or fp32.
  *   FP8  : out = fl(e4m3(q) * s)
  *   NVFP4: out = fl(fl(e2m1(q) * e4m3(s_b)) * s_t)   (the inner product is exact)
+ *   MX   : out = e2m1 / e4m3(q) * 2^(e-127)                  (exact in fp32)
  * bf16 output is the RNE rounding of that fp32 value. out is dense
- * [rows, cols]. NVFP4 needs cols % 16 == 0.
+ * [rows, cols]. NVFP4 needs cols % 16 == 0. MX needs cols % 32 == 0, a NULL
+ * tensor_scale, 16-byte aligned out and codes aligned to 4 (MXFP4) or 8
+ * (MXFP8) bytes.
  */
 qg_status qg_dequant(qg_format fmt, const void *codes, const void *block_scales,
                      const float *tensor_scale, int64_t rows, int64_t cols,

@@ -18,7 +18,8 @@ from dataclasses import dataclass
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqgemm.so")
 
-QG_FMT_BF16, QG_FMT_FP8_E4M3, QG_FMT_NVFP4 = 0, 1, 2
+QG_FMT_BF16, QG_FMT_FP8_E4M3, QG_FMT_NVFP4, QG_FMT_MXFP4, QG_FMT_MXFP8 = 0, 1, 2, 3, 4
+MX_FORMATS = (QG_FMT_MXFP4, QG_FMT_MXFP8)
 QG_OUT_BF16, QG_OUT_F32 = 0, 1
 QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
@@ -155,7 +156,8 @@ def qg_abi_version() -> int:
 # ---------------------------------------------------------------- allocating helpers
 @dataclass
 class QTensor:
-    """A quantized tensor on the GPU: codes, block scales (NVFP4) and the fp32 tensor scale."""
+    """A quantized tensor on the GPU: codes, block scales (NVFP4, MX) and the
+    fp32 tensor scale (None for the MX formats, which have none)."""
     fmt: int
     codes: "object"
     block_scales: "object"
@@ -175,10 +177,16 @@ def quantize(x, fmt: int, stream=None, static_scale=None) -> QTensor:
     if fmt == QG_FMT_FP8_E4M3:
         codes = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
         bs = None
+    elif fmt in MX_FORMATS:
+        codes = torch.empty((rows, cols if fmt == QG_FMT_MXFP8 else cols // 2), dtype=torch.uint8, device=dev)
+        bs = torch.empty((rows, cols // 32), dtype=torch.uint8, device=dev)
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
         bs = torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev)
     ldx = x.stride(0) if rows > 1 else cols   # a size-1 dimension may carry any stride
+    if fmt in MX_FORMATS:
+        qg_quantize_act(fmt, x, rows, cols, ldx, codes, bs, None, stream)
+        return QTensor(fmt, codes, bs, None, rows, cols)
     if static_scale is not None:
         qg_quantize_act_static(fmt, x, rows, cols, ldx, codes, bs, static_scale, stream)
         return QTensor(fmt, codes, bs, static_scale, rows, cols)
@@ -205,8 +213,8 @@ def unpack(packed, fmt: int, n: int, k: int, stream=None) -> QTensor:
         codes, bs = torch.empty((n, k), dtype=torch.uint8, device=dev), None
     else:
         codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev)
-        bs = torch.empty((n, k // 16), dtype=torch.uint8, device=dev)
-    ts = torch.empty(1, dtype=torch.float32, device=dev)
+        bs = torch.empty((n, k // (32 if fmt == QG_FMT_MXFP4 else 16)), dtype=torch.uint8, device=dev)
+    ts = None if fmt == QG_FMT_MXFP4 else torch.empty(1, dtype=torch.float32, device=dev)
     qg_unpack_weights(fmt, packed, packed.numel(), n, k, codes, bs, ts, stream)
     return QTensor(fmt, codes, bs, ts, n, k)
 

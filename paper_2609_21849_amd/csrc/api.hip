@@ -23,7 +23,15 @@ qg_status hip_status(hipError_t e) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-bool valid_fmt(int f) { return f == QG_FMT_BF16 || f == QG_FMT_FP8_E4M3 || f == QG_FMT_NVFP4; }
+bool valid_fmt(int f) {
+  return f == QG_FMT_BF16 || f == QG_FMT_FP8_E4M3 || f == QG_FMT_NVFP4 || f == QG_FMT_MXFP4 || f == QG_FMT_MXFP8;
+}
+
+bool is_mx(int f) { return f == QG_FMT_MXFP4 || f == QG_FMT_MXFP8; }
+
+// MX element codes: 4-byte stores / loads of 8 MXFP4 codes, 8-byte ones of
+// 8 MXFP8 codes
+uintptr_t mx_code_align(int f) { return f == QG_FMT_MXFP4 ? 4 : 8; }
 
 constexpr int64_t kMaxDim = std::numeric_limits<int32_t>::max();
 
@@ -53,6 +61,18 @@ qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t co
   if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
   if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
+  if (is_mx(fmt)) {  // block scales only: no tensor scale
+    if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
+    if (cols % 32 != 0) return QG_ERR_SHAPE;
+    if (rows > 0 && cols > 0 &&
+        (x == nullptr || codes == nullptr || block_scales == nullptr || !aligned(x, 2) ||
+         !aligned(codes, fmt == QG_FMT_MXFP4 ? 4 : 1)))
+      return QG_ERR_INVALID_ARG;
+    return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
+                                          reinterpret_cast<uint8_t*>(codes),
+                                          reinterpret_cast<uint8_t*>(block_scales), nullptr,
+                                          reinterpret_cast<hipStream_t>(stream)));
+  }
   if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
   if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
   if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
@@ -70,7 +90,7 @@ qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t co
 qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
                                  void* codes, void* block_scales, const float* tensor_scale, void* stream) {
   if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (fmt == QG_FMT_BF16 || is_mx(fmt)) return QG_ERR_UNSUPPORTED;
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
   if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
   if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
@@ -87,8 +107,9 @@ qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int
 }
 
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k) {
-  if (fmt != QG_FMT_FP8_E4M3 && fmt != QG_FMT_NVFP4) return 0;
+  if (fmt != QG_FMT_FP8_E4M3 && fmt != QG_FMT_NVFP4 && fmt != QG_FMT_MXFP4) return 0;
   if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim || n % 16 != 0 || k % 128 != 0) return 0;
+  if (fmt == QG_FMT_MXFP4 && k % 256 != 0) return 0;
   return (size_t)qg::packed_total_bytes((int)fmt, n, k);
 }
 
@@ -96,15 +117,19 @@ static qg_status check_pack_args(qg_format fmt, const void* codes, const void* b
                                  const void* tensor_scale, int64_t n, int64_t k,
                                  const void* packed, size_t packed_bytes) {
   if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (fmt == QG_FMT_BF16 || fmt == QG_FMT_MXFP8) return QG_ERR_UNSUPPORTED;
   if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
   if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
-  if (packed == nullptr || tensor_scale == nullptr || !aligned(packed, 256) || !aligned(tensor_scale, 4))
+  if (fmt == QG_FMT_MXFP4 && k % 256 != 0) return QG_ERR_SHAPE;
+  if (packed == nullptr || !aligned(packed, 256)) return QG_ERR_INVALID_ARG;
+  // MXFP4 has no tensor scale; the others carry one in the header
+  if (fmt == QG_FMT_MXFP4 ? tensor_scale != nullptr : (tensor_scale == nullptr || !aligned(tensor_scale, 4)))
     return QG_ERR_INVALID_ARG;
   if (packed_bytes < (size_t)qg::packed_total_bytes((int)fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
   if (n > 0 && k > 0) {
     if (codes == nullptr || !aligned(codes, 16)) return QG_ERR_INVALID_ARG;
     if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(block_scales, 8))) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_MXFP4 && block_scales == nullptr) return QG_ERR_INVALID_ARG;
   }
   if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
   return QG_OK;
@@ -141,9 +166,11 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   const bool w8a8 = (a_fmt == QG_FMT_FP8_E4M3 && w_fmt == QG_FMT_FP8_E4M3);
   const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
   const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
-  if (!(w8a8 || w4a4 || w4a16)) return QG_ERR_UNSUPPORTED;
+  const bool mx4 = (a_fmt == QG_FMT_MXFP4 && w_fmt == QG_FMT_MXFP4);
+  if (!(w8a8 || w4a4 || w4a16 || mx4)) return QG_ERR_UNSUPPORTED;
   if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
   if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
+  if (mx4 && k % 256 != 0) return QG_ERR_SHAPE;
   if (m > 0 && lda < k) return QG_ERR_INVALID_ARG;
   if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
   if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
@@ -151,7 +178,7 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   // operands are addressed with 32-bit byte offsets: every operand extent
   // (activation rows, their block scales, the packed weight) must stay below 2 GiB
   if (m > 0 && k > 0) {
-    const int64_t esz2 = w8a8 ? 2 : (w4a4 ? 1 : 4);  // element size x 2
+    const int64_t esz2 = w8a8 ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
     const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
     if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
   }
@@ -166,6 +193,9 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
                    !aligned(a_block_scales, 8)))
         return QG_ERR_INVALID_ARG;
       if (w4a16 && (!aligned(a, 16) || lda % 8 != 0 || a_tensor_scale != nullptr || a_block_scales != nullptr))
+        return QG_ERR_INVALID_ARG;
+      if (mx4 && (!aligned(a, 16) || lda != k || a_tensor_scale != nullptr || a_block_scales == nullptr ||
+                  !aligned(a_block_scales, 8)))
         return QG_ERR_INVALID_ARG;
     }
   }
@@ -182,6 +212,17 @@ qg_status qg_dequant(qg_format fmt, const void* codes, const void* block_scales,
   if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
   if (out_dtype != QG_OUT_BF16 && out_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (is_mx(fmt)) {
+    if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
+    if (cols % 32 != 0) return QG_ERR_SHAPE;
+    if (rows > 0 && cols > 0 &&
+        (codes == nullptr || block_scales == nullptr || out == nullptr || !aligned(codes, mx_code_align(fmt)) ||
+         !aligned(out, 16)))
+      return QG_ERR_INVALID_ARG;
+    return hip_status(qg::launch_dequant((int)fmt, reinterpret_cast<const uint8_t*>(codes),
+                                         reinterpret_cast<const uint8_t*>(block_scales), nullptr, rows, cols,
+                                         out, out_dtype == QG_OUT_F32, reinterpret_cast<hipStream_t>(stream)));
+  }
   if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
   if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
   if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;

@@ -1185,6 +1185,264 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------------- MXFP4 (W4A4, MX block scaling)
+// OCP MXFP4 x MXFP4 on gfx950's block-scaled matrix instruction:
+// v_mfma_scale_f32_32x32x64_f8f6f4 with fp4 operands takes, per lane, 32
+// E2M1 codes (16 bytes: lanes 0-31 reduction elements 0-31 of the step,
+// lanes 32-63 elements 32-63) and one E8M0 scale byte for them -- exactly
+// one MX block -- so the format runs at the fp4 matrix rate with no operand
+// expansion at all. Same tiles and waves as k_gemm_fp8_direct (256 x 256,
+// four waves of 128 x 128, persistent grid, staged epilogue); the reduction
+// advances in chunks of 256 (4 MFMA steps of 64, 64 MFMAs of 32 cycles per
+// wave per chunk):
+//   weights     : one 1 KiB code image per panel and step, loaded straight
+//                 into registers three steps ahead (a ring of four steps,
+//                 refilled right after each step's last use), plus one dword
+//                 per panel and chunk holding the lane's four block scales;
+//   activations : 128 bytes per row and chunk staged in LDS (piece c = step
+//                 s = c / 2, lane half g = c % 2; the 16-byte slot of lane
+//                 32 g + row is XOR-ed with 2 s + 9 g, so that the 8 pieces
+//                 of a row, written by 8 neighbouring lanes, and any 16
+//                 neighbouring lanes' reads fall into distinct bank groups
+//                 for 32 and 64 banks alike), the row's 8 block scales
+//                 re-ordered while staging so that a lane reads its 4 as one
+//                 dword; the MFMA's byte select picks step s's scale. A group
+//                 of 4 fp4 MFMAs lasts about one LDS read latency, so the
+//                 fragments are read two groups ahead.
+// K must be a multiple of 256 (checked by the caller).
+__global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
+  constexpr int A_CODES = 8 * 4096;              // 8 panels x 4 steps x 1 KiB
+  constexpr int A_STAGE = A_CODES + 256 * 8;     // + 8 scale bytes per row
+  constexpr int OUT_STAGE = 32 * (64 * 4 + 16);
+  constexpr uint32_t OOB = 0x80000000u;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t sout[4 * OUT_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 31, gq = lane >> 5;
+  const int kcn = g.k >> 8;                      // chunks of 256
+  const int steps = g.k >> 6;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const uint32_t ka = (uint32_t)(g.k >> 1), ks = (uint32_t)(g.k >> 5);  // A code / scale bytes per row
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * ka), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a_bscale), 0, (int)((int64_t)g.m * ks), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * steps * 1024), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_bs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
+
+  uint32_t oa[8], la[8], osa, ob[4], osb[4];
+  v4i ga[8];           // staged activation codes of a chunk
+  uint2 gs;            // staged activation scales of the thread's row
+  v4i fb[4][4];        // weight codes, ring over steps: [step % 4][panel]
+  uint32_t bsc[2][4];  // weight scales [chunk parity][panel]: byte s = step s
+  uint32_t asc[2][4];  // activation scales [chunk parity][panel]: byte s = step s
+  v4i fa[4];           // activation fragments, ring over MFMA groups (read two groups ahead)
+  v16f acc[4][4];
+
+  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  auto load_a = [&](int kc) __attribute__((always_inline)) {
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int it = 0; it < 8; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[it] + kc * 128) | hi, 0, 0);
+    const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + kc * 8) | hi, 0, 0);
+    gs = make_uint2((uint32_t)t.x, (uint32_t)t.y);
+  };
+  // row scales of the chunk, blocks 0..7 -> [half 0: 0 2 4 6][half 1: 1 3 5 7]
+  auto write_a_scales = [&](uint8_t* st) __attribute__((always_inline)) {
+    const uint32_t lo = __builtin_amdgcn_perm(gs.y, gs.x, 0x06040200u);
+    const uint32_t hi = __builtin_amdgcn_perm(gs.y, gs.x, 0x07050301u);
+    *reinterpret_cast<uint2*>(st + A_CODES + tid * 8) = make_uint2(lo, hi);
+  };
+  // weight codes of global step t (= 4 x chunk + step) into ring slot S
+  auto load_b = [&](auto Sc, int t) __attribute__((always_inline)) {
+    constexpr int S = decltype(Sc)::value;
+    const uint32_t hi = t < steps ? 0u : OOB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[S][j] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, (ob[j] + t * 1024) | hi, 0, 0);
+  };
+  auto load_bs = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bsc[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + kc * 256) | hi, 0, 0);
+  };
+  auto read_fa = [&](const uint8_t* st, int s, int i) __attribute__((always_inline)) {
+    return *reinterpret_cast<const v4i*>(st + (wm * 4 + i) * 4096 + s * 1024 + ((lane ^ (2 * s + 9 * gq)) * 16));
+  };
+  auto read_asc = [&](auto Pc, const uint8_t* st) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      asc[P][i] = *reinterpret_cast<const uint32_t*>(st + A_CODES + ((wm * 4 + i) * 32 + r) * 8 + 4 * gq);
+  };
+  // MFMA group f = (step f / 4, activation panel f % 4) on fragment fa[f % 4]
+  auto mgroup = [&](auto Pc, auto Fc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value, f = decltype(Fc)::value;
+    const v4i xa = fa[f & 3];
+    const v8i xv = (v8i){xa.x, xa.y, xa.z, xa.w, 0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const v4i wa = fb[f >> 2][j];
+      const v8i wv = (v8i){wa.x, wa.y, wa.z, wa.w, 0, 0, 0, 0};
+      acc[f & 3][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wv, xv, acc[f & 3][j], 4, 4, f >> 2, (int)bsc[P][j],
+                                                                       f >> 2, (int)asc[P][f & 3]);
+    }
+  };
+  // one region: groups 4s .. 4s + NG - 1, each a fragment read for the next
+  // group and 4 MFMAs; NV global loads and NW LDS writes spread over the slots
+  auto pattern = [&](auto NGc, auto NVc, auto NWc) __attribute__((always_inline)) {
+    constexpr int NG = decltype(NGc)::value, NV = decltype(NVc)::value, NW = decltype(NWc)::value;
+#pragma unroll
+    for (int f = 0; f < NG; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (4 * f + t < NW) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+        if (4 * f + t < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // fragment reads run two groups ahead of their MFMAs: group f reads the
+  // fragment of group f + 2 (for f = 14, 15: groups 0, 1 of the next chunk,
+  // after the barrier that publishes it)
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    using I = std::integral_constant<int, 0>;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    const int t0 = 4 * kc;
+    // step 0: refill slot 3 (step 3 of this chunk)
+    load_b(std::integral_constant<int, 3>(), t0 + 3);
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 2) & 3] = read_fa(cur, (F + 2) >> 2, (F + 2) & 3), mgroup(Pc, std::integral_constant<int, F>())), ...);
+    }(std::make_integer_sequence<int, 4>());
+    pattern(std::integral_constant<int, 4>(), std::integral_constant<int, 4>(), I());
+    // step 1: slot 0 <- step 0 of the next chunk; next chunk's weight scales
+    load_b(std::integral_constant<int, 0>(), t0 + 4);
+    load_bs(std::integral_constant<int, P ^ 1>(), kc + 1);
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 6) & 3] = read_fa(cur, (F + 6) >> 2, (F + 6) & 3), mgroup(Pc, std::integral_constant<int, F + 4>())), ...);
+    }(std::make_integer_sequence<int, 4>());
+    pattern(std::integral_constant<int, 4>(), std::integral_constant<int, 8>(), I());
+    // step 2: slot 1 refill; stage the activations of chunk kc + 1 (written
+    // between the fragment reads in program order), then load those of kc + 2
+    const uint32_t a_hi = past(kc + 2);
+    load_b(std::integral_constant<int, 1>(), t0 + 5);
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 10) & 3] = read_fa(cur, (F + 10) >> 2, (F + 10) & 3),
+        *reinterpret_cast<v4i*>(nxt + la[2 * F]) = ga[2 * F],
+        *reinterpret_cast<v4i*>(nxt + la[2 * F + 1]) = ga[2 * F + 1],
+        mgroup(Pc, std::integral_constant<int, F + 8>()),
+        ga[2 * F] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[2 * F] + (kc + 2) * 128) | a_hi, 0, 0),
+        ga[2 * F + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[2 * F + 1] + (kc + 2) * 128) | a_hi, 0, 0)), ...);
+    }(std::make_integer_sequence<int, 4>());
+    pattern(std::integral_constant<int, 4>(), std::integral_constant<int, 12>(), std::integral_constant<int, 8>());
+    // step 3, first half: slot 2 refill, the row scales of chunk kc + 1
+    load_b(std::integral_constant<int, 2>(), t0 + 6);
+    write_a_scales(nxt);
+    {
+      const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + (kc + 2) * 8) | a_hi, 0, 0);
+      gs = make_uint2((uint32_t)t.x, (uint32_t)t.y);
+    }
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 14) & 3] = read_fa(cur, 3, (F + 2) & 3), mgroup(Pc, std::integral_constant<int, F + 12>())), ...);
+    }(std::make_integer_sequence<int, 2>());
+    pattern(std::integral_constant<int, 2>(), std::integral_constant<int, 5>(), std::integral_constant<int, 1>());
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // step 3, second half: the next chunk's first two fragments and its scales
+    fa[0] = read_fa(nxt, 0, 0);
+    mgroup(Pc, std::integral_constant<int, 14>());
+    fa[1] = read_fa(nxt, 0, 1);
+    read_asc(std::integral_constant<int, P ^ 1>(), nxt);
+    mgroup(Pc, std::integral_constant<int, 15>());
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 256, n0 = bn * 256;
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int q = it * 256 + tid;
+      const int p = q >> 8, rr = (q >> 3) & 31, c = q & 7;
+      const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
+      oa[it] = (row < (uint32_t)g.m) ? row * ka + 16u * c : OOB;
+      la[it] = (uint32_t)(p * 4096 + (c >> 1) * 1024 + (((rr + 32 * (c & 1)) ^ (2 * (c >> 1) + 9 * (c & 1))) * 16));
+    }
+    {
+      const uint32_t row = (uint32_t)(m0 + tid);
+      osa = (row < (uint32_t)g.m) ? row * ks : OOB;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 4 + j);
+      const bool in = panel < (uint32_t)npanels_w;
+      ob[j] = in ? panel * (uint32_t)(steps * 1024) + 16u * lane : OOB;
+      osb[j] = in ? panel * (uint32_t)(kcn * 256) + 4u * lane : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    int kc = 0;
+    if (kcn & 1) {  // odd chunk count: first chunk unpipelined
+      load_a(0);
+      load_b(std::integral_constant<int, 0>(), 0);
+      load_b(std::integral_constant<int, 1>(), 1);
+      load_b(std::integral_constant<int, 2>(), 2);
+      load_b(std::integral_constant<int, 3>(), 3);
+      load_bs(std::integral_constant<int, 0>(), 0);
+#pragma unroll
+      for (int it = 0; it < 8; ++it) *reinterpret_cast<v4i*>(smem + la[it]) = ga[it];
+      write_a_scales(smem);
+      __syncthreads();
+      read_asc(std::integral_constant<int, 0>(), smem);
+      [&]<int... F>(std::integer_sequence<int, F...>) {
+        ((fa[F & 3] = read_fa(smem, F >> 2, F & 3), mgroup(std::integral_constant<int, 0>(), std::integral_constant<int, F>())), ...);
+      }(std::make_integer_sequence<int, 16>());
+      __syncthreads();
+      kc = 1;
+    }
+    if (kc < kcn) {
+      load_a(kc);
+#pragma unroll
+      for (int it = 0; it < 8; ++it) *reinterpret_cast<v4i*>(smem + la[it]) = ga[it];
+      write_a_scales(smem);
+      __syncthreads();
+      load_a(kc + 1);
+      load_b(std::integral_constant<int, 0>(), 4 * kc);
+      load_b(std::integral_constant<int, 1>(), 4 * kc + 1);
+      load_b(std::integral_constant<int, 2>(), 4 * kc + 2);
+      load_bs(std::integral_constant<int, 0>(), kc);
+      fa[0] = read_fa(smem, 0, 0);
+      fa[1] = read_fa(smem, 0, 1);
+      read_asc(std::integral_constant<int, 0>(), smem);
+      for (; kc < kcn; kc += 2) {
+        chunk(std::integral_constant<int, 0>(), kc);
+        chunk(std::integral_constant<int, 1>(), kc + 1);
+      }
+    }
+    // no tensor scales in MX: the block scales are applied inside the MFMAs
+    if (fast_out && m0 + 256 <= g.m && n0 + 256 <= g.n)
+      store_tiles_fast<4, 4>(g, acc, sout + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, 1.0f);
+    else
+      store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, 1.0f);
+  }
+}
+
 // ---------------------------------------------------------------- W4A16, up to 1024 tokens
 // bf16 activations against NVFP4 weights when the output is too small to
 // fill the chip with large tiles (the text-encoder linears). A workgroup
@@ -1504,7 +1762,7 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, m, n, ldy, (int)f32out);
     return hipGetLastError();
   }
-  const int w_fmt = (a_fmt == 1) ? 1 : 2;
+  const int w_fmt = (a_fmt == 1) ? 1 : (a_fmt == 3) ? 3 : 2;
   GemmArgs g;
   g.a = reinterpret_cast<const uint8_t*>(a);
   g.a_bscale = a_bscale;
@@ -1520,8 +1778,14 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   g.ldy = ldy;
   g.f32out = f32out ? 1 : 0;
   g.tiles_m = g.tiles_n = 0;
-  // Large tiles: 256 x 256 per workgroup, 8 wavefronts (two per SIMD, so
-  // one wave's MFMAs cover the other's LDS and barrier waits), 128 x 64 each.
+  // persistent grids of 256 x 256 tiles, four waves of 128 x 128 each
+  if (a_fmt == 3) {
+    g.tiles_m = (g.m + 255) / 256;
+    g.tiles_n = (g.n + 255) / 256;
+    const int tiles = g.tiles_m * g.tiles_n;
+    hipLaunchKernelGGL(k_gemm_mxfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    return hipGetLastError();
+  }
   if (a_fmt == 1) {
     if (m <= 128) return run_fp8<1, 2>(g, st);
     g.tiles_m = (g.m + 255) / 256;

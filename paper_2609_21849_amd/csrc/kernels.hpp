@@ -1,6 +1,7 @@
 // kernels.hpp -- internal launchers shared by the C-ABI layer (api.hip).
 // Each launcher only enqueues work on `st`; arguments were validated by the
-// caller. Format ids follow qg_format: 0 bf16, 1 FP8 E4M3, 2 NVFP4.
+// caller. Format ids follow qg_format: 0 bf16, 1 FP8 E4M3, 2 NVFP4,
+// 3 MXFP4, 4 MXFP8.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -11,7 +12,7 @@
 namespace qg {
 
 // Packed weight buffer: a 256-byte header, then the codes region, then (for
-// NVFP4) the block-scale region. Header fields (little endian):
+// NVFP4 and MXFP4) the block-scale region. Header fields (little endian):
 //   +0 u32 magic 'QGPW', +4 u32 layout version, +8 u32 format,
 //   +16 i64 n, +24 i64 k, +32 f32 tensor decode scale.
 // The weight is stored in panels of 32 rows (n rounded up to a multiple of
@@ -26,8 +27,11 @@ inline int64_t padded_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPane
 inline int64_t packed_codes_bytes(int fmt, int64_t n, int64_t k) {
   return fmt == 1 ? padded_rows(n) * k : padded_rows(n) * k / 2;
 }
+inline int64_t packed_scale_bytes(int fmt, int64_t n, int64_t k) {
+  return fmt == 2 ? padded_rows(n) * k / 16 : fmt == 3 ? padded_rows(n) * k / 32 : 0;
+}
 inline int64_t packed_total_bytes(int fmt, int64_t n, int64_t k) {
-  return kPackHeader + packed_codes_bytes(fmt, n, k) + (fmt == 2 ? padded_rows(n) * k / 16 : 0);
+  return kPackHeader + packed_codes_bytes(fmt, n, k) + packed_scale_bytes(fmt, n, k);
 }
 
 hipError_t launch_quantize_static(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,

@@ -14,8 +14,15 @@
 //          64 t + 32 g + 16 h (each step is one self-contained MFMA operand);
 //   NVFP4: 2048-byte code chunk, piece h of lane l = row r, bytes 32 g + 16 h;
 //          block scales in their own region, 256 bytes per chunk = [row][8].
+//   MXFP4: per 64-wide step t one 1024-byte image [lane][16 B], lane l = row
+//          r, elements 64 t + 32 g .. + 31 (bytes 32 t + 16 g): exactly one
+//          32-element scale block per lane, the operand of a scaled fp4 MFMA;
+//          E8M0 scales in their own region, per 256-wide chunk c one run of
+//          4 bytes per lane = the scales of the lane's blocks in steps
+//          4c .. 4c + 3 (blocks 8c + 2s + g), read as one dword per lane.
 // Chunks of one panel follow each other along k, so a panel is one
-// contiguous stream. The header keeps format, n, k and the tensor scale.
+// contiguous stream. The header keeps format, n, k and the tensor scale
+// (1.0 for MXFP4, which has none).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -29,16 +36,24 @@ __global__ void k_pack_header(uint8_t* packed, int fmt, int64_t n, int64_t k, co
   h[3] = 0u;
   reinterpret_cast<int64_t*>(packed)[2] = n;
   reinterpret_cast<int64_t*>(packed)[3] = k;
-  reinterpret_cast<float*>(packed + kPackScaleOffset)[0] = *tscale;
+  reinterpret_cast<float*>(packed + kPackScaleOffset)[0] = tscale ? *tscale : 1.0f;
 }
 
 __global__ void k_unpack_header(const uint8_t* packed, float* tscale) {
-  *tscale = reinterpret_cast<const float*>(packed + kPackScaleOffset)[0];
+  if (tscale) *tscale = reinterpret_cast<const float*>(packed + kPackScaleOffset)[0];
 }
 
 // Canonical [n, row_bytes] byte offset of the 16-byte piece that packed
 // piece `p` holds, or -1 for a padding row (see the layout above).
 __device__ inline int64_t canon_piece(int fmt, int64_t p, int64_t n, int64_t k) {
+  if (fmt == 3) {
+    const int64_t steps = k / 64;
+    const int64_t sc = p >> 6, l = p & 63;
+    const int64_t panel = sc / steps, t = sc - panel * steps;
+    const int64_t row = panel * 32 + (l & 31);
+    if (row >= n) return -1;
+    return row * (k / 2) + t * 32 + 16 * (l >> 5);
+  }
   const int64_t kc_n = k / 128;
   const int per = (fmt == 1) ? 256 : 128;            // pieces per chunk
   const int64_t chunk = p / per, s = p - chunk * per;
@@ -87,6 +102,29 @@ __global__ void __launch_bounds__(256) k_pack_scales(uint8_t* canon, uint8_t* pa
     *reinterpret_cast<uint2*>(canon + c) = reinterpret_cast<const uint2*>(packed_scales)[p];
 }
 
+// MXFP4 scale runs: run p = (panel, 256-wide chunk c, lane l); byte s of
+// the run is the E8M0 scale of block 8c + 2s + g of row panel * 32 + r.
+template <bool PACK>
+__global__ void __launch_bounds__(256) k_pack_mx_scales(uint8_t* canon, uint8_t* packed_scales,
+                                                        int64_t nruns, int64_t n, int64_t k) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= nruns) return;
+  const int64_t cn = k / 256;
+  const int64_t pc = p >> 6, l = p & 63;
+  const int64_t panel = pc / cn, c = pc - panel * cn;
+  const int64_t row = panel * 32 + (l & 31), g = l >> 5;
+  uint8_t* run = packed_scales + 4 * p;
+  if (PACK) {
+    uint32_t w = 0;
+    if (row < n)
+      for (int s = 0; s < 4; ++s) w |= (uint32_t)canon[row * (k / 32) + 8 * c + 2 * s + g] << (8 * s);
+    *reinterpret_cast<uint32_t*>(run) = w;
+  } else if (row < n) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(run);
+    for (int s = 0; s < 4; ++s) canon[row * (k / 32) + 8 * c + 2 * s + g] = (uint8_t)(w >> (8 * s));
+  }
+}
+
 static inline unsigned blocks_for(int64_t t) { return (unsigned)((t + 255) / 256); }
 
 hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, const float* tscale,
@@ -98,6 +136,11 @@ hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, con
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<true>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt,
                      const_cast<uint8_t*>(codes), pc, npieces, n, k);
+  if (fmt == 3) {
+    const int64_t nruns = padded_rows(n) * k / 128;
+    hipLaunchKernelGGL(k_pack_mx_scales<true>, dim3(blocks_for(nruns)), dim3(256), 0, st,
+                       const_cast<uint8_t*>(bscale), pc + cb, nruns, n, k);
+  }
   if (fmt == 2) {
     const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_scales<true>, dim3(blocks_for(nruns)), dim3(256), 0, st,
@@ -115,6 +158,11 @@ hipError_t launch_unpack(int fmt, const uint8_t* packed, int64_t n, int64_t k, u
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<false>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt, codes,
                      pc, npieces, n, k);
+  if (fmt == 3) {
+    const int64_t nruns = padded_rows(n) * k / 128;
+    hipLaunchKernelGGL(k_pack_mx_scales<false>, dim3(blocks_for(nruns)), dim3(256), 0, st, bscale,
+                       pc + cb, nruns, n, k);
+  }
   if (fmt == 2) {
     const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_scales<false>, dim3(blocks_for(nruns)), dim3(256), 0, st, bscale,

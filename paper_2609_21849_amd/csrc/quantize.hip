@@ -292,6 +292,71 @@ __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict_
   }
 }
 
+// ---------------------------------------------------------------- MX formats
+// OCP MX (MXFP4: E2M1 elements, MXFP8: E4M3 elements), one E8M0 scale per 32
+// consecutive elements of a row, no tensor scale: the block scaling gfx950's
+// matrix cores consume natively. Shared exponent = floor(log2 max|x|) - emax
+// (emax 2 for E2M1, 8 for E4M3), E8M0 code = that + 127 clamped to [0, 254],
+// 0 for an all-zero block; elements = RNE_sat(x * 2^(127 - code)), the
+// multiply exact (a power of two, inside the normal range for bf16 inputs).
+// One thread codes 8 consecutive elements of a row; rows hold whole blocks
+// (cols % 32 == 0), so the 4 threads of a block are lanes 4j .. 4j + 3 of one
+// wave and share its max with two lane swaps. VEC: 16-byte aligned rows.
+template <bool FP4, bool VEC>
+__global__ void __launch_bounds__(256) k_quant_mx(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                  int64_t ldx, uint8_t* __restrict__ q,
+                                                  uint8_t* __restrict__ scales) {
+  const int64_t upr = cols >> 3;  // 8-element units per row
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool live = u < rows * upr;
+  const int64_t row = live ? u / upr : 0, c8 = live ? u - row * upr : 0;
+  float v[8];
+  if (live) {
+    const uint16_t* p = x + row * ldx + 8 * c8;
+    if (VEC) {
+      const uint4 w = *reinterpret_cast<const uint4*>(p);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[2 * j] = bf16_lo(ww[j]);
+        v[2 * j + 1] = bf16_hi(ww[j]);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = u2f((uint32_t)p[j] << 16);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = 0.0f;
+  }
+  uint32_t am = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
+  am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+  am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+  // floor(log2(max)) from the fp32 bits (normal or denormal), then the code
+  int e = 0;
+  if (am != 0u) {
+    const int ef = (int)(am >> 23);
+    const int fl = (ef > 0) ? ef - 127 : (31 - __builtin_clz(am)) - 149;
+    e = min(max(fl - (FP4 ? 2 : 8) + 127, 0), 254);
+  }
+  const float r = u2f((uint32_t)(254 - e) << 23);  // 2^(127 - e), e <= 252 here
+  float y[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
+  if (!live) return;
+  if (FP4) {
+    *reinterpret_cast<uint32_t*>(q + row * (cols >> 1) + 4 * c8) = hw_e2m1x8(y);
+  } else {
+    const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
+    uint8_t* d = q + row * cols + 8 * c8;
+    if ((reinterpret_cast<uintptr_t>(d) & 7) == 0) *reinterpret_cast<uint2*>(d) = make_uint2(lo, hi);
+    else for (int j = 0; j < 8; ++j) d[j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
+  }
+  if ((c8 & 3) == 0) scales[row * (cols >> 5) + (c8 >> 2)] = (uint8_t)e;
+}
+
 // ---------------------------------------------------------------- dequant
 // out = fl(e4m3(q) * s)  or  fl(fl(e2m1(q) * e4m3(s_b)) * s_t), as fp32 or
 // RNE bf16; one thread per 16 consecutive elements of the dense tensor.
@@ -359,6 +424,36 @@ __global__ void __launch_bounds__(256) k_dequant_nvfp4(const uint8_t* __restrict
   store16<F32OUT>(out, b * 16, v, 16, vec);
 }
 
+// MX: out = element * 2^(e - 127) (exact in fp32), one thread per 8 elements.
+template <bool FP4, bool F32OUT>
+__global__ void __launch_bounds__(256) k_dequant_mx(const uint8_t* __restrict__ q, const uint8_t* __restrict__ sc,
+                                                    int64_t n, void* __restrict__ out) {
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (u * 8 >= n) return;
+  const uint32_t e = sc[u >> 2];
+  const float scale = (e == 0u) ? u2f(0x00400000u) : u2f(e << 23);  // 2^(e - 127)
+  float v[8];
+  if (FP4) {
+    const uint32_t w = reinterpret_cast<const uint32_t*>(q)[u];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = dec_e2m1((w >> (4 * j)) & 15u) * scale;
+  } else {
+    const uint2 w = reinterpret_cast<const uint2*>(q)[u];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = dec_e4m3(((j < 4 ? w.x : w.y) >> (8 * (j & 3))) & 0xFFu) * scale;
+  }
+  if (F32OUT) {
+    float4* o = reinterpret_cast<float4*>(out) + 2 * u;
+    o[0] = make_float4(v[0], v[1], v[2], v[3]);
+    o[1] = make_float4(v[4], v[5], v[6], v[7]);
+  } else {
+    uint32_t h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) h[j] = f32_to_bf16(v[2 * j]) | (f32_to_bf16(v[2 * j + 1]) << 16);
+    reinterpret_cast<uint4*>(out)[u] = make_uint4(h[0], h[1], h[2], h[3]);
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 static inline unsigned grid_for(int64_t threads) { return (unsigned)((threads + 255) / 256); }
 
@@ -403,8 +498,25 @@ hipError_t launch_quantize_static(int fmt, const uint16_t* x, int64_t rows, int6
   return hipGetLastError();
 }
 
+// MX formats: block scales only, one kernel.
+static hipError_t launch_quantize_mx(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
+                                     uint8_t* codes, uint8_t* scales, hipStream_t st) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const unsigned g = grid_for(rows * (cols / 8));
+  const bool vec = (reinterpret_cast<uintptr_t>(x) % 16 == 0) && (ldx % 8 == 0);
+  if (fmt == 3) {
+    if (vec) hipLaunchKernelGGL((k_quant_mx<true, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, scales);
+    else hipLaunchKernelGGL((k_quant_mx<true, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, scales);
+  } else {
+    if (vec) hipLaunchKernelGGL((k_quant_mx<false, true>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, scales);
+    else hipLaunchKernelGGL((k_quant_mx<false, false>), dim3(g), dim3(256), 0, st, x, rows, cols, ldx, codes, scales);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ldx,
                            uint8_t* codes, uint8_t* bscale, float* tscale, hipStream_t st) {
+  if (fmt == 3 || fmt == 4) return launch_quantize_mx(fmt, x, rows, cols, ldx, codes, bscale, st);
   if (rows == 0 || cols == 0) {
     hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(1), 0, st, reinterpret_cast<uint32_t*>(tscale), 0u);
     return hipGetLastError();
@@ -452,6 +564,17 @@ hipError_t launch_dequant(int fmt, const uint8_t* codes, const uint8_t* bscale, 
                           int64_t rows, int64_t cols, void* out, bool f32out, hipStream_t st) {
   const int64_t n = rows * cols;
   if (n == 0) return hipSuccess;
+  if (fmt == 3 || fmt == 4) {  // MX: aligned buffers (checked by the caller)
+    const unsigned g = grid_for(n / 8);
+    if (fmt == 3) {
+      if (f32out) hipLaunchKernelGGL((k_dequant_mx<true, true>), dim3(g), dim3(256), 0, st, codes, bscale, n, out);
+      else hipLaunchKernelGGL((k_dequant_mx<true, false>), dim3(g), dim3(256), 0, st, codes, bscale, n, out);
+    } else {
+      if (f32out) hipLaunchKernelGGL((k_dequant_mx<false, true>), dim3(g), dim3(256), 0, st, codes, bscale, n, out);
+      else hipLaunchKernelGGL((k_dequant_mx<false, false>), dim3(g), dim3(256), 0, st, codes, bscale, n, out);
+    }
+    return hipGetLastError();
+  }
   if (fmt == 1) {
     const bool vec = (reinterpret_cast<uintptr_t>(codes) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(out) % 16 == 0);

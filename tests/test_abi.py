@@ -156,3 +156,66 @@ def test_dequant_validation():
     assert dq(NVFP4, out=None) == INVALID
     assert dq(FP8) == INVALID                                            # FP8 with block scales
     assert dq(NVFP4, out=P + 2, od=1) == INVALID                          # fp32 out alignment
+
+
+MXFP4, MXFP8 = q.QG_FMT_MXFP4, q.QG_FMT_MXFP8
+
+
+def test_mx_packed_bytes():
+    # header + E2M1 codes + one E8M0 scale per 32 elements
+    assert q.qg_packed_bytes(MXFP4, 64, 256) == 256 + 64 * 256 // 2 + 64 * 256 // 32
+    assert q.qg_packed_bytes(MXFP4, 48, 512) == 256 + 64 * 512 // 2 + 64 * 512 // 32   # 32-row panels
+    assert q.qg_packed_bytes(MXFP4, 64, 128) == 0     # MXFP4 weights need k % 256
+    assert q.qg_packed_bytes(MXFP8, 64, 256) == 0     # MXFP8 weights are not packable
+
+
+def test_mx_quantize_validation():
+    assert _quant(MXFP4) == INVALID                                   # MX has no tensor scale
+    assert _quant(MXFP8) == INVALID
+    assert _quant(MXFP4, ts=None, cols=48, ldx=48) == SHAPE           # cols % 32
+    assert _quant(MXFP8, ts=None, cols=16, ldx=16) == SHAPE
+    assert _quant(MXFP4, ts=None, bs=None) == INVALID                 # block scales required
+    assert _quant(MXFP4, ts=None, codes=P + 2) == INVALID             # 4-byte code stores
+    assert _quant(MXFP4, ts=None, x=None) == INVALID
+    assert _quant(MXFP4, ts=None, x=P + 1) == INVALID
+    assert _quant(MXFP8, ts=None, ldx=16) == INVALID                  # ldx < cols
+    assert _quant_static(MXFP4) == UNSUP                              # no static MX scale
+    assert _quant_static(MXFP8, ts=None) == UNSUP
+
+
+@pytest.mark.parametrize("unpack", [False, True])
+def test_mx_pack_validation(unpack):
+    assert _pack(MXFP8, ts=None, k=256, unpack=unpack) == UNSUP
+    assert _pack(MXFP4, ts=None, k=128, unpack=unpack) == SHAPE       # k % 256
+    assert _pack(MXFP4, ts=None, n=24, k=256, unpack=unpack) == SHAPE
+    assert _pack(MXFP4, k=256, unpack=unpack) == INVALID              # no tensor scale
+    assert _pack(MXFP4, ts=None, bs=None, k=256, unpack=unpack) == INVALID
+    assert _pack(MXFP4, ts=None, k=256, nbytes=4000, unpack=unpack) == SMALL
+
+
+def test_mx_gemm_validation():
+    mx = dict(a_fmt=MXFP4, w_fmt=MXFP4, ats=None)
+    assert _gemm(a_fmt=MXFP4, w_fmt=NVFP4, ats=None) == UNSUP
+    assert _gemm(a_fmt=NVFP4, w_fmt=MXFP4) == UNSUP
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8, ats=None) == UNSUP
+    assert _gemm(a_fmt=BF16, w_fmt=MXFP4, abs_=None, ats=None) == UNSUP
+    assert _gemm(**mx, k=384, lda=384) == SHAPE                       # k % 256
+    assert _gemm(a_fmt=MXFP4, w_fmt=MXFP4) == INVALID                 # MX A has no tensor scale
+    assert _gemm(**mx, abs_=None) == INVALID                          # A block scales required
+    assert _gemm(**mx, abs_=P + 4) == INVALID                         # 8-byte aligned scales
+    assert _gemm(**mx, lda=512) == INVALID                            # dense codes
+    assert _gemm(**mx, a=P + 8) == INVALID
+    assert _gemm(**mx, m=70000, k=65536, lda=65536) == SHAPE          # codes above 2 GiB
+
+
+def test_mx_dequant_validation():
+    def dq(fmt, codes=P, bs=P, ts=None, rows=4, cols=64, out=P, od=1):
+        return q.qg_dequant(fmt, codes, bs, ts, rows, cols, out, od, stream=0, check=False)
+    assert dq(MXFP4, ts=P) == INVALID                                 # no tensor scale
+    assert dq(MXFP4, cols=48) == SHAPE
+    assert dq(MXFP8, cols=16) == SHAPE
+    assert dq(MXFP4, bs=None) == INVALID
+    assert dq(MXFP4, out=None) == INVALID
+    assert dq(MXFP4, out=P + 8) == INVALID                            # 16-byte stores
+    assert dq(MXFP4, codes=P + 2) == INVALID                          # 4-byte code loads
+    assert dq(MXFP8, codes=P + 4) == INVALID                          # 8-byte code loads

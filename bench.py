@@ -333,6 +333,7 @@ def main():
     parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
     parts["mxfp4"] = mxfp4_part(q, lib, st, dit, M, flops, parts["nvfp4"])
     parts["dit_block_chain"] = block_chain_part(q, dit, M)
+    parts["weight_streaming"] = weight_streaming_part(q, dit, M)
     parts["w8a8_encoder"] = w8a8_encoder_part(q, enc)
     parts["w4a16_cold_pool"] = w4a16_pool(q, synth, args.pool_mib)
 
@@ -522,6 +523,129 @@ def mxfp4_part(q, lib, st, dit, M, flops, nvfp4, steps=10):
             "rel_err_vs_unquantized": rel,
             "note": "MXFP4 is the matrix-core-native 4-bit format (power-of-two scales per 32); its "
                     "outputs differ from NVFP4's by design and are checked against their own oracle"}
+
+
+def weight_streaming_part(q, dit, M, blocks=8, steps=3):
+    """Weight streaming (the paper's second memory tool): a transformer of
+    `blocks` blocks x the four linears, its packed weights in pinned host
+    memory, run through qg_run_layers with the resident subset chosen by
+    qg_stream_plan for a range of device budgets. Reports the measured
+    host-to-device rate M, the per-linear compute L (quantize + GEMM), the
+    reservoir decay factor lambda = L M / W of each linear, T_min, and per
+    budget the planned and measured step times. Every block reuses the same
+    four weights (one device copy, one pinned host copy each): residency only
+    changes where the bytes come from, so this times the schedule, not the
+    weights."""
+    import ctypes
+    import torch
+    lib = q.lib()
+    comp = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    out = {}
+    for kind, fmt in (("fp8", q.QG_FMT_FP8_E4M3), ("nvfp4", q.QG_FMT_NVFP4)):
+        host = {}
+        for e in dit:
+            w = e["w_" + kind]
+            h = torch.empty(w.numel(), dtype=torch.uint8, pin_memory=True)
+            h.copy_(w)
+            host[e["name"]] = h
+        # host-to-device rate on the copy stream (largest weight, 5 copies)
+        big = max(dit, key=lambda e: e["w_" + kind].numel())
+        dst = torch.empty_like(big["w_" + kind])
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        with torch.cuda.stream(copy):
+            dst.copy_(host[big["name"]], non_blocking=True)
+            ev[0].record()
+            for _ in range(5):
+                dst.copy_(host[big["name"]], non_blocking=True)
+            ev[1].record()
+        torch.cuda.synchronize()
+        rate = 5 * dst.numel() / (ev[0].elapsed_time(ev[1]) * 1e-3)
+
+        def layer_list(resident):
+            L = []
+            for b in range(blocks):
+                for j, e in enumerate(dit):
+                    a = e["a_" + kind]
+                    r = int(resident[b * len(dit) + j])
+                    w = e["w_" + kind] if r else host[e["name"]]
+                    L.append(q.StreamLayer(
+                        x=e["x"][kind].data_ptr(), a_fmt=fmt, a_codes=a.codes.data_ptr(),
+                        a_block_scales=a.block_scales.data_ptr() if a.block_scales is not None else None,
+                        a_tensor_scale=a.tensor_scale.data_ptr(), w_fmt=fmt, w_packed=w.data_ptr(),
+                        w_packed_bytes=w.numel(), resident=r, m=M, n=e["n"], k=e["k"],
+                        y=e["y_" + kind].data_ptr(), y_dtype=q.QG_OUT_BF16))
+            return L
+
+        nl = blocks * len(dit)
+        wb = [float(dit[i % len(dit)]["w_" + kind].numel()) for i in range(nl)]
+        slot_bytes = (int(max(wb)) + 255) // 256 * 256
+        slots = [torch.empty(slot_bytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+        evr, evf = [], []
+        for _ in range(2):
+            for lst in (evr, evf):
+                e_ = torch.cuda.Event()
+                e_.record()
+                lst.append(e_)
+        cursor = ctypes.c_int32(0)
+
+        def run(resident, n_steps):
+            layers = layer_list(resident)
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for i in range(n_steps + 1):
+                if i == 1:
+                    t0.record()
+                q.qg_run_layers(layers, slots, slot_bytes, [x.cuda_event for x in evr], [x.cuda_event for x in evf],
+                                cursor, compute_stream=comp, copy_stream=copy)
+            t1.record()
+            torch.cuda.synchronize()
+            return t0.elapsed_time(t1) / n_steps * 1e-3
+
+        # per-linear compute time (quantize + GEMM) from a fully resident single block
+        lin_s = {}
+        for j, e in enumerate(dit):
+            one = layer_list([1] * nl)[j:j + 1]
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            q.qg_run_layers(one, [], 0, [], [], ctypes.c_int32(0), compute_stream=comp, copy_stream=copy)
+            s0.record()
+            for _ in range(10):
+                q.qg_run_layers(one, [], 0, [], [], ctypes.c_int32(0), compute_stream=comp, copy_stream=copy)
+            s1.record()
+            torch.cuda.synchronize()
+            lin_s[e["name"]] = s0.elapsed_time(s1) / 10 * 1e-3
+        cs = [lin_s[dit[i % len(dit)]["name"]] for i in range(nl)]
+        a_max = float(max(M * e["k"] * 2 + M * e["n"] * 2 for e in dit))   # bf16 input + output of a linear
+        tmin = 2 * max(wb) + a_max
+        full = sum(wb) + a_max
+        plans = {}
+        for label, budget in (("resident_100", full), ("resident_75", a_max + 0.75 * sum(wb)),
+                              ("resident_50", a_max + 0.5 * sum(wb)), ("resident_25", a_max + 0.25 * sum(wb)),
+                              ("t_min", tmin)):
+            budget = max(budget, tmin)
+            st_, res, pred, dev = q.qg_stream_plan(wb, cs, 2, rate, budget, a_max)
+            meas = run(res, steps)
+            plans[label] = {"budget_mb": round(budget / 1e6, 1), "device_mb": round(dev / 1e6, 1),
+                            "resident_layers": int(sum(res)), "streamed_layers": nl - int(sum(res)),
+                            "predicted_ms": round(pred * 1e3, 3), "measured_ms": round(meas * 1e3, 3)}
+        # the two ends: every weight resident, every weight streamed
+        plans["all_resident"] = {"device_mb": round(full / 1e6, 1), "resident_layers": nl, "streamed_layers": 0,
+                                 "predicted_ms": round(sum(cs) * 1e3, 3),
+                                 "measured_ms": round(run([1] * nl, steps) * 1e3, 3)}
+        _, pred_all = q.qg_stream_simulate(wb, cs, [0] * nl, 2, rate, 3)
+        plans["all_streamed"] = {"device_mb": round(tmin / 1e6, 1), "resident_layers": 0, "streamed_layers": nl,
+                                 "predicted_ms": round(pred_all * 1e3, 3),
+                                 "measured_ms": round(run([0] * nl, steps) * 1e3, 3)}
+        lam = {dit[j]["name"]: round(cs[(j - 1) % len(dit)] * rate / wb[j], 3) for j in range(len(dit))}
+        out[kind] = {"layers": nl, "h2d_gbs": round(rate / 1e9, 1),
+                     "linear_us": {k_: round(v * 1e6, 1) for k_, v in lin_s.items()},
+                     "weight_mb": {e["name"]: round(e["w_" + kind].numel() / 1e6, 2) for e in dit},
+                     "lambda": lam, "t_min_mb": round(tmin / 1e6, 1), "all_resident_mb": round(full / 1e6, 1),
+                     "delta_all_streamed_ms": round(sum(wb) / rate * 1e3, 3),
+                     "plans": plans}
+    out["note"] = ("lambda = L M / W with L the compute of the preceding linear; delta_all_streamed = N W / M, the "
+                   "paper's overhead bound with no overlapped layer; predicted = qg_stream_simulate of the plan with "
+                   "the measured L and M")
+    return out
 
 
 def static_scale_part(q, lib, st, dit, M, flops, steps=10):

@@ -225,6 +225,93 @@ qg_status qg_dequant(qg_format fmt, const void *codes, const void *block_scales,
                      const float *tensor_scale, int64_t rows, int64_t cols,
                      void *out, qg_out_dtype out_dtype, void *stream);
 
+/*
+ * ---------------------------------------------------------------- weight streaming
+ * Paper: Sec. 4, weight-streaming paragraph. A resident subset of the layer
+ * weights stays in device memory; the other packed weights live in pinned
+ * host memory and are copied into a few device buffers ("slots") ahead of
+ * their GEMM, on a copy stream, so that the copies overlap the compute. Only
+ * where the weight bytes come from changes: the outputs are bit-identical to
+ * a run with every weight resident. The paper's model of the cost:
+ *   lambda = L * M / W   (L: compute time between successive GEMMs, M: the
+ *                         host-to-device rate, W: the layer's weight bytes);
+ *   lambda >= 1 hides every copy; lambda < 1 adds up to Delta = (N-K) W / M
+ *   (N layers, K overlapped); device memory cannot go below
+ *   T_min = 2 W_max + A_max (two slots of the largest streamed layer plus
+ *   the peak activation).
+ */
+
+/* One linear of a streamed run: optional activation quantization, then the
+ * GEMM. Field meanings are those of qg_quantize_act and qg_gemm. */
+typedef struct qg_stream_layer {
+    const void *x;            /* bf16 [m, k] dense input (lda = k) */
+    qg_format a_fmt;          /* BF16: x is the GEMM operand; else x is quantized first */
+    void *a_codes;            /* quantize outputs (device), unused for BF16 */
+    void *a_block_scales;
+    float *a_tensor_scale;    /* NULL for MXFP4 */
+    qg_format w_fmt;
+    const void *w_packed;     /* resident: device buffer; streamed: host buffer (pinned for overlap) */
+    size_t w_packed_bytes;
+    int32_t resident;         /* nonzero: w_packed is device memory used in place */
+    int64_t m, n, k;
+    void *y;                  /* [m, n] output, ldy = n */
+    qg_out_dtype y_dtype;
+} qg_stream_layer;
+
+/*
+ * qg_run_layers -- enqueue one pass over `layers` in order. For every layer:
+ * (quantize x on compute_stream), then, if it is streamed, the copy of its
+ * packed weight into slot s = *slot_cursor (then s + 1 mod n_slots) on
+ * copy_stream after slot_free[s] (the slot's previous GEMM), followed by
+ * slot_ready[s]; the GEMM waits for slot_ready[s] on compute_stream and
+ * records slot_free[s]. Nothing waits on the host.
+ *   slots       n_slots device buffers of slot_bytes each, 256-byte aligned
+ *               (slot_bytes >= every streamed layer's w_packed_bytes).
+ *   slot_ready, slot_free  n_slots hipEvent_t each, created by the caller
+ *               (hipEventDisableTiming is fine) and reused across calls.
+ *   slot_cursor in/out: the slot the first streamed layer takes; repeated
+ *               calls (one per step) keep the round robin going.
+ *   compute_stream, copy_stream  hipStream_t (distinct for overlap).
+ * Every layer's arguments are checked before anything is enqueued, with the
+ * checks and status codes of qg_quantize_act and qg_gemm. n_slots must be
+ * >= 1 when a layer is streamed.
+ */
+qg_status qg_run_layers(const qg_stream_layer *layers, int32_t n_layers,
+                        void *const *slots, int32_t n_slots, size_t slot_bytes,
+                        void *const *slot_ready, void *const *slot_free, int32_t *slot_cursor,
+                        void *compute_stream, void *copy_stream);
+
+/*
+ * qg_stream_simulate -- the schedule qg_run_layers enqueues, as a
+ * discrete-event model: layers in order, `steps` passes; the streamed
+ * occurrences take the n_slots slots in turn; one copy engine at
+ * h2d_bytes_per_s serves the copies in order; a copy starts once its slot's
+ * previous layer has computed; a layer computes once the previous one has
+ * finished and its weight is in place (compute_s[i] seconds).
+ *   step_s  out: the duration of the last pass (the steady state for
+ *           steps >= 3).
+ * Pure host arithmetic (no GPU).
+ */
+qg_status qg_stream_simulate(int32_t n_layers, const double *w_bytes, const double *compute_s,
+                             const uint8_t *resident, int32_t n_slots, double h2d_bytes_per_s,
+                             int32_t steps, double *step_s);
+
+/*
+ * qg_stream_plan -- choose the resident layers for a device memory budget.
+ * Device bytes of a plan = resident weights + n_slots x the largest streamed
+ * weight + act_peak_bytes. The plan minimises the simulated step time
+ * (qg_stream_simulate, 3 passes), then the device bytes: over every resident
+ * subset for up to 16 layers; for more layers, for each slot size (every
+ * layer above it resident) layers are made resident greedily by step time
+ * saved per byte while they fit and copies are still exposed.
+ *   resident_out  n_layers flags; step_s, device_bytes: of the chosen plan.
+ * QG_ERR_BUFFER_TOO_SMALL when no plan fits (budget below T_min and below
+ * the all-resident size). Pure host arithmetic (no GPU).
+ */
+qg_status qg_stream_plan(int32_t n_layers, const double *w_bytes, const double *compute_s, int32_t n_slots,
+                         double h2d_bytes_per_s, double budget_bytes, double act_peak_bytes,
+                         uint8_t *resident_out, double *step_s, double *device_bytes);
+
 /* Human-readable name of a status code (static storage, never NULL). */
 const char *qg_status_string(qg_status s);
 

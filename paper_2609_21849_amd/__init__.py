@@ -25,7 +25,17 @@ QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
                 4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
 EXPORTS = ["qg_quantize_act", "qg_quantize_act_static", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
-           "qg_dequant", "qg_status_string", "qg_last_hip_error", "qg_abi_version"]
+           "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
+           "qg_last_hip_error", "qg_abi_version"]
+
+
+class StreamLayer(ctypes.Structure):
+    """qg_stream_layer of include/qgemm.h."""
+    _fields_ = [("x", ctypes.c_void_p), ("a_fmt", ctypes.c_int), ("a_codes", ctypes.c_void_p),
+                ("a_block_scales", ctypes.c_void_p), ("a_tensor_scale", ctypes.c_void_p),
+                ("w_fmt", ctypes.c_int), ("w_packed", ctypes.c_void_p), ("w_packed_bytes", ctypes.c_size_t),
+                ("resident", ctypes.c_int32), ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("y", ctypes.c_void_p), ("y_dtype", ctypes.c_int)]
 
 
 class QGError(RuntimeError):
@@ -60,6 +70,15 @@ def lib() -> ctypes.CDLL:
         L.qg_gemm.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, I32, P]
         L.qg_dequant.restype = I32
         L.qg_dequant.argtypes = [I32, P, P, P, I64, I64, P, I32, P]
+        D, U8 = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_uint8)
+        L.qg_run_layers.restype = I32
+        L.qg_run_layers.argtypes = [ctypes.POINTER(StreamLayer), ctypes.c_int32, ctypes.POINTER(P), ctypes.c_int32, SZ,
+                                    ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(ctypes.c_int32), P, P]
+        L.qg_stream_simulate.restype = I32
+        L.qg_stream_simulate.argtypes = [ctypes.c_int32, D, D, U8, ctypes.c_int32, ctypes.c_double, ctypes.c_int32, D]
+        L.qg_stream_plan.restype = I32
+        L.qg_stream_plan.argtypes = [ctypes.c_int32, D, D, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_double, U8, D, D]
         L.qg_status_string.restype = ctypes.c_char_p
         L.qg_status_string.argtypes = [I32]
         L.qg_last_hip_error.restype = I32
@@ -132,6 +151,52 @@ def qg_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_pa
     if check:
         _check(s, "qg_gemm")
     return s
+
+
+def _doubles(v):
+    arr = (ctypes.c_double * max(1, len(v)))(*[float(x) for x in v])
+    return arr
+
+
+def qg_run_layers(layers, slots, slot_bytes, slot_ready, slot_free, slot_cursor, compute_stream=None,
+                  copy_stream=None, check=True):
+    """layers: sequence of StreamLayer; slots: device pointers (ints or
+    tensors); slot_ready / slot_free: hipEvent_t handles (ints, e.g.
+    torch.cuda.Event.cuda_event); slot_cursor: a ctypes.c_int32, updated."""
+    arr = (StreamLayer * max(1, len(layers)))(*layers)
+    n_slots = len(slots)
+    sp = (ctypes.c_void_p * max(1, n_slots))(*[_p(t) for t in slots])
+    rp = (ctypes.c_void_p * max(1, n_slots))(*slot_ready)
+    fp = (ctypes.c_void_p * max(1, n_slots))(*slot_free)
+    s = lib().qg_run_layers(arr, len(layers), sp, n_slots, slot_bytes, rp, fp, ctypes.byref(slot_cursor),
+                            _stream(compute_stream), _stream(copy_stream))
+    if check:
+        _check(s, "qg_run_layers")
+    return s
+
+
+def qg_stream_simulate(w_bytes, compute_s, resident, n_slots, h2d_bytes_per_s, steps=3, check=True):
+    """Returns (status, step seconds of the last pass)."""
+    n = len(w_bytes)
+    res = (ctypes.c_uint8 * max(1, n))(*[1 if r else 0 for r in resident])
+    out = ctypes.c_double(0.0)
+    s = lib().qg_stream_simulate(n, _doubles(w_bytes), _doubles(compute_s), res, n_slots, h2d_bytes_per_s, steps,
+                                 ctypes.byref(out))
+    if check:
+        _check(s, "qg_stream_simulate")
+    return s, out.value
+
+
+def qg_stream_plan(w_bytes, compute_s, n_slots, h2d_bytes_per_s, budget_bytes, act_peak_bytes, check=True):
+    """Returns (status, resident flags, step seconds, device bytes)."""
+    n = len(w_bytes)
+    res = (ctypes.c_uint8 * max(1, n))()
+    t, b = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    s = lib().qg_stream_plan(n, _doubles(w_bytes), _doubles(compute_s), n_slots, h2d_bytes_per_s, budget_bytes,
+                             act_peak_bytes, res, ctypes.byref(t), ctypes.byref(b))
+    if check:
+        _check(s, "qg_stream_plan")
+    return s, [int(res[i]) for i in range(n)], t.value, b.value
 
 
 def qg_dequant(fmt, codes, block_scales, tensor_scale, rows, cols, out, out_dtype, stream=None, check=True):

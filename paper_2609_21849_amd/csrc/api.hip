@@ -8,6 +8,7 @@
 
 #include <limits>
 
+#include "checks.hpp"
 #include "kernels.hpp"
 #include "qgemm.h"
 
@@ -37,6 +38,81 @@ constexpr int64_t kMaxDim = std::numeric_limits<int32_t>::max();
 
 }  // namespace
 
+namespace qg {
+
+qg_status check_quantize(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
+                         const void* codes, const void* block_scales, const float* tensor_scale) {
+  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
+  const bool empty = (rows == 0 || cols == 0);
+  if (is_mx(fmt)) {  // block scales only: no tensor scale
+    if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
+    if (cols % 32 != 0) return QG_ERR_SHAPE;
+    if (!empty && (x == nullptr || codes == nullptr || block_scales == nullptr || !aligned(x, 2) ||
+                   !aligned(codes, fmt == QG_FMT_MXFP4 ? 4 : 1)))
+      return QG_ERR_INVALID_ARG;
+    return QG_OK;
+  }
+  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+  if (!empty) {
+    if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+  }
+  return QG_OK;
+}
+
+qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales, const float* a_tensor_scale,
+                     int64_t lda, qg_format w_fmt, const void* w_packed, size_t w_packed_bytes, int64_t m,
+                     int64_t n, int64_t k, const void* y, int64_t ldy, qg_out_dtype y_dtype) {
+  if (!valid_fmt(a_fmt) || !valid_fmt(w_fmt)) return QG_ERR_INVALID_ARG;
+  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+  const bool w8a8 = (a_fmt == QG_FMT_FP8_E4M3 && w_fmt == QG_FMT_FP8_E4M3);
+  const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
+  const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
+  const bool mx4 = (a_fmt == QG_FMT_MXFP4 && w_fmt == QG_FMT_MXFP4);
+  if (!(w8a8 || w4a4 || w4a16 || mx4)) return QG_ERR_UNSUPPORTED;
+  if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
+  if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
+  if (mx4 && k % 256 != 0) return QG_ERR_SHAPE;
+  if (m > 0 && lda < k) return QG_ERR_INVALID_ARG;
+  if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
+  if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
+  if (w_packed_bytes < (size_t)packed_total_bytes((int)w_fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
+  // operands are addressed with 32-bit byte offsets: every operand extent
+  // (activation rows, their block scales, the packed weight) must stay below 2 GiB
+  if (m > 0 && k > 0) {
+    const int64_t esz2 = w8a8 ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
+    const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
+    if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
+  }
+  if (packed_total_bytes((int)w_fmt, n, k) > kMaxDim) return QG_ERR_SHAPE;
+  if (m > 0 && n > 0) {
+    if (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2)) return QG_ERR_INVALID_ARG;
+    if (k > 0) {
+      if (a == nullptr) return QG_ERR_INVALID_ARG;
+      if (w8a8 && (!aligned(a, 16) || lda % 16 != 0 || a_tensor_scale == nullptr || a_block_scales != nullptr))
+        return QG_ERR_INVALID_ARG;
+      if (w4a4 && (!aligned(a, 16) || lda != k || a_tensor_scale == nullptr || a_block_scales == nullptr ||
+                   !aligned(a_block_scales, 8)))
+        return QG_ERR_INVALID_ARG;
+      if (w4a16 && (!aligned(a, 16) || lda % 8 != 0 || a_tensor_scale != nullptr || a_block_scales != nullptr))
+        return QG_ERR_INVALID_ARG;
+      if (mx4 && (!aligned(a, 16) || lda != k || a_tensor_scale != nullptr || a_block_scales == nullptr ||
+                  !aligned(a_block_scales, 8)))
+        return QG_ERR_INVALID_ARG;
+    }
+  }
+  return QG_OK;
+}
+
+qg_status status_of(hipError_t e) { return hip_status(e); }
+
+}  // namespace qg
+
 extern "C" {
 
 const char* qg_status_string(qg_status s) {
@@ -57,34 +133,12 @@ int qg_abi_version(void) { return QG_ABI_VERSION; }
 
 qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
                           void* codes, void* block_scales, float* tensor_scale, void* stream) {
-  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
-  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
-  if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
-  if (is_mx(fmt)) {  // block scales only: no tensor scale
-    if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
-    if (cols % 32 != 0) return QG_ERR_SHAPE;
-    if (rows > 0 && cols > 0 &&
-        (x == nullptr || codes == nullptr || block_scales == nullptr || !aligned(x, 2) ||
-         !aligned(codes, fmt == QG_FMT_MXFP4 ? 4 : 1)))
-      return QG_ERR_INVALID_ARG;
-    return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
-                                          reinterpret_cast<uint8_t*>(codes),
-                                          reinterpret_cast<uint8_t*>(block_scales), nullptr,
-                                          reinterpret_cast<hipStream_t>(stream)));
-  }
-  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
-  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
-  const bool empty = (rows == 0 || cols == 0);
-  if (!empty) {
-    if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
-    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
-  }
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols,
-                                        ldx, reinterpret_cast<uint8_t*>(codes),
-                                        reinterpret_cast<uint8_t*>(block_scales), tensor_scale, st));
+  const qg_status c = qg::check_quantize(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale);
+  if (c != QG_OK) return c;
+  return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
+                                        reinterpret_cast<uint8_t*>(codes),
+                                        reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                        reinterpret_cast<hipStream_t>(stream)));
 }
 
 qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
@@ -161,44 +215,9 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
                   const float* a_tensor_scale, int64_t lda, qg_format w_fmt, const void* w_packed,
                   size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y, int64_t ldy,
                   qg_out_dtype y_dtype, void* stream) {
-  if (!valid_fmt(a_fmt) || !valid_fmt(w_fmt)) return QG_ERR_INVALID_ARG;
-  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
-  const bool w8a8 = (a_fmt == QG_FMT_FP8_E4M3 && w_fmt == QG_FMT_FP8_E4M3);
-  const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
-  const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
-  const bool mx4 = (a_fmt == QG_FMT_MXFP4 && w_fmt == QG_FMT_MXFP4);
-  if (!(w8a8 || w4a4 || w4a16 || mx4)) return QG_ERR_UNSUPPORTED;
-  if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
-  if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
-  if (mx4 && k % 256 != 0) return QG_ERR_SHAPE;
-  if (m > 0 && lda < k) return QG_ERR_INVALID_ARG;
-  if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
-  if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
-  if (w_packed_bytes < (size_t)qg::packed_total_bytes((int)w_fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
-  // operands are addressed with 32-bit byte offsets: every operand extent
-  // (activation rows, their block scales, the packed weight) must stay below 2 GiB
-  if (m > 0 && k > 0) {
-    const int64_t esz2 = w8a8 ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
-    const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
-    if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
-  }
-  if (qg::packed_total_bytes((int)w_fmt, n, k) > kMaxDim) return QG_ERR_SHAPE;
-  if (m > 0 && n > 0) {
-    if (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2)) return QG_ERR_INVALID_ARG;
-    if (k > 0) {
-      if (a == nullptr) return QG_ERR_INVALID_ARG;
-      if (w8a8 && (!aligned(a, 16) || lda % 16 != 0 || a_tensor_scale == nullptr || a_block_scales != nullptr))
-        return QG_ERR_INVALID_ARG;
-      if (w4a4 && (!aligned(a, 16) || lda != k || a_tensor_scale == nullptr || a_block_scales == nullptr ||
-                   !aligned(a_block_scales, 8)))
-        return QG_ERR_INVALID_ARG;
-      if (w4a16 && (!aligned(a, 16) || lda % 8 != 0 || a_tensor_scale != nullptr || a_block_scales != nullptr))
-        return QG_ERR_INVALID_ARG;
-      if (mx4 && (!aligned(a, 16) || lda != k || a_tensor_scale != nullptr || a_block_scales == nullptr ||
-                  !aligned(a_block_scales, 8)))
-        return QG_ERR_INVALID_ARG;
-    }
-  }
+  const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
+                                     w_packed_bytes, m, n, k, y, ldy, y_dtype);
+  if (c != QG_OK) return c;
   return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
                                     a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
                                     n, k, y, ldy, y_dtype == QG_OUT_F32,

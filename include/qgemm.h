@@ -148,8 +148,8 @@ qg_status qg_quantize_act_static(qg_format fmt, const void *x, int64_t rows, int
 
 /*
  * qg_packed_bytes -- size of the packed weight buffer for an [n, k] weight
- * in `fmt` (FP8, NVFP4 or MXFP4), or 0 when the shape breaks the GEMM
- * contract (n % 16, k % 128; MXFP4 k % 256) or the format is not packable.
+ * in `fmt` (FP8, NVFP4, MXFP4 or MXFP8), or 0 when the shape breaks the GEMM
+ * contract (n % 16, k % 128; MX k % 256) or the format is not packable.
  */
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
 
@@ -161,11 +161,11 @@ size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
  * like the cached engines of Sec. 5).
  *
  *   codes, block_scales, tensor_scale: as written by qg_quantize_act
- *                 (block_scales NULL for FP8; tensor_scale NULL for MXFP4).
+ *                 (block_scales NULL for FP8; tensor_scale NULL for MX).
  *   packed        out: qg_packed_bytes(fmt, n, k) bytes, 256-byte aligned.
  * The layout is private to this library version (qg_unpack_weights is its
- * exact inverse). Shapes: n % 16 == 0 and k % 128 == 0 (MXFP4: k % 256),
- * else QG_ERR_SHAPE. MXFP8 weights are not packable: QG_ERR_UNSUPPORTED.
+ * exact inverse). Shapes: n % 16 == 0 and k % 128 == 0 (MX: k % 256), else
+ * QG_ERR_SHAPE.
  */
 qg_status qg_pack_weights(qg_format fmt, const void *codes, const void *block_scales,
                           const float *tensor_scale, int64_t n, int64_t k,
@@ -193,6 +193,9 @@ qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_byt
  *                         (8-byte aligned, lda = k), a_tensor_scale NULL;
  *                         k % 256 == 0. The E8M0 block scales of both
  *                         operands are applied by the matrix instruction.
+ *   (MXFP8,    MXFP8)     MX W8A8: a = codes [m, k], a_block_scales [m, k/32]
+ *                         (4-byte aligned, lda = k), a_tensor_scale NULL;
+ *                         k % 256 == 0.
  *   a_tensor_scale  device fp32 decode scale of A (FP8, NVFP4).
  *   w_packed        buffer written by qg_pack_weights for an [n, k] weight.
  *   y               out: [m, ldy] of y_dtype.

@@ -276,10 +276,13 @@ def unpack(packed, fmt: int, n: int, k: int, stream=None) -> QTensor:
     dev = packed.device
     if fmt == QG_FMT_FP8_E4M3:
         codes, bs = torch.empty((n, k), dtype=torch.uint8, device=dev), None
+    elif fmt in MX_FORMATS:
+        codes = torch.empty((n, k if fmt == QG_FMT_MXFP8 else k // 2), dtype=torch.uint8, device=dev)
+        bs = torch.empty((n, k // 32), dtype=torch.uint8, device=dev)
     else:
         codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev)
-        bs = torch.empty((n, k // (32 if fmt == QG_FMT_MXFP4 else 16)), dtype=torch.uint8, device=dev)
-    ts = None if fmt == QG_FMT_MXFP4 else torch.empty(1, dtype=torch.float32, device=dev)
+        bs = torch.empty((n, k // 16), dtype=torch.uint8, device=dev)
+    ts = None if fmt in MX_FORMATS else torch.empty(1, dtype=torch.float32, device=dev)
     qg_unpack_weights(fmt, packed, packed.numel(), n, k, codes, bs, ts, stream)
     return QTensor(fmt, codes, bs, ts, n, k)
 

@@ -74,10 +74,11 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
   const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
   const bool mx4 = (a_fmt == QG_FMT_MXFP4 && w_fmt == QG_FMT_MXFP4);
-  if (!(w8a8 || w4a4 || w4a16 || mx4)) return QG_ERR_UNSUPPORTED;
+  const bool mx8 = (a_fmt == QG_FMT_MXFP8 && w_fmt == QG_FMT_MXFP8);
+  if (!(w8a8 || w4a4 || w4a16 || mx4 || mx8)) return QG_ERR_UNSUPPORTED;
   if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
   if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
-  if (mx4 && k % 256 != 0) return QG_ERR_SHAPE;
+  if ((mx4 || mx8) && k % 256 != 0) return QG_ERR_SHAPE;
   if (m > 0 && lda < k) return QG_ERR_INVALID_ARG;
   if (m > 0 && ldy < n) return QG_ERR_INVALID_ARG;
   if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
@@ -85,7 +86,7 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   // operands are addressed with 32-bit byte offsets: every operand extent
   // (activation rows, their block scales, the packed weight) must stay below 2 GiB
   if (m > 0 && k > 0) {
-    const int64_t esz2 = w8a8 ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
+    const int64_t esz2 = (w8a8 || mx8) ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
     const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
     if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
   }
@@ -103,6 +104,9 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
         return QG_ERR_INVALID_ARG;
       if (mx4 && (!aligned(a, 16) || lda != k || a_tensor_scale != nullptr || a_block_scales == nullptr ||
                   !aligned(a_block_scales, 8)))
+        return QG_ERR_INVALID_ARG;
+      if (mx8 && (!aligned(a, 16) || lda != k || a_tensor_scale != nullptr || a_block_scales == nullptr ||
+                  !aligned(a_block_scales, 4)))
         return QG_ERR_INVALID_ARG;
     }
   }
@@ -161,9 +165,9 @@ qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int
 }
 
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k) {
-  if (fmt != QG_FMT_FP8_E4M3 && fmt != QG_FMT_NVFP4 && fmt != QG_FMT_MXFP4) return 0;
+  if (!valid_fmt(fmt) || fmt == QG_FMT_BF16) return 0;
   if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim || n % 16 != 0 || k % 128 != 0) return 0;
-  if (fmt == QG_FMT_MXFP4 && k % 256 != 0) return 0;
+  if (is_mx(fmt) && k % 256 != 0) return 0;
   return (size_t)qg::packed_total_bytes((int)fmt, n, k);
 }
 
@@ -171,19 +175,19 @@ static qg_status check_pack_args(qg_format fmt, const void* codes, const void* b
                                  const void* tensor_scale, int64_t n, int64_t k,
                                  const void* packed, size_t packed_bytes) {
   if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16 || fmt == QG_FMT_MXFP8) return QG_ERR_UNSUPPORTED;
+  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
   if (n < 0 || k < 0 || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
   if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
-  if (fmt == QG_FMT_MXFP4 && k % 256 != 0) return QG_ERR_SHAPE;
+  if (is_mx(fmt) && k % 256 != 0) return QG_ERR_SHAPE;
   if (packed == nullptr || !aligned(packed, 256)) return QG_ERR_INVALID_ARG;
-  // MXFP4 has no tensor scale; the others carry one in the header
-  if (fmt == QG_FMT_MXFP4 ? tensor_scale != nullptr : (tensor_scale == nullptr || !aligned(tensor_scale, 4)))
+  // the MX formats have no tensor scale; the others carry one in the header
+  if (is_mx(fmt) ? tensor_scale != nullptr : (tensor_scale == nullptr || !aligned(tensor_scale, 4)))
     return QG_ERR_INVALID_ARG;
   if (packed_bytes < (size_t)qg::packed_total_bytes((int)fmt, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
   if (n > 0 && k > 0) {
     if (codes == nullptr || !aligned(codes, 16)) return QG_ERR_INVALID_ARG;
     if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(block_scales, 8))) return QG_ERR_INVALID_ARG;
-    if (fmt == QG_FMT_MXFP4 && block_scales == nullptr) return QG_ERR_INVALID_ARG;
+    if (is_mx(fmt) && block_scales == nullptr) return QG_ERR_INVALID_ARG;
   }
   if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
   return QG_OK;

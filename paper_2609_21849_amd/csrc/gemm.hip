@@ -703,20 +703,28 @@ __device__ __attribute__((always_inline)) inline void store_tiles_fast(const Gem
 // as 8 panels of 4 KiB. Piece c (bytes 16c .. 16c+15 of the row's chunk)
 // belongs to step s = c / 4, lane half g = (c / 2) % 2 and register half
 // h = c % 2 of the MFMA operand, so it lands in 1 KiB block 2s + h of its
-// panel at slot (r + 32 g) ^ c: the eight lanes of a row spread over banks,
-// and the operand read of lane l (slot l ^ (4s + 2g + h)) is a permutation of
-// one contiguous 1 KiB block -- conflict free.
+// panel at slot (r + 32 g) ^ (c + 8 h): the eight lanes of a row, and the
+// sixteen lanes of two rows, fall into distinct bank groups (32 or 64
+// banks), and the operand read of lane l (slot l ^ (4s + 2g + 9h)) is a
+// permutation of one contiguous 1 KiB block -- conflict free.
+//
+// MX8 (MXFP8): the block-scaled fp8 instruction reads a row's scale block h
+// from register half h of both lane halves, so there piece c belongs to
+// step s = c / 4, register half h = (c / 2) % 2 and lane half g = c % 2; the
+// slot XOR is the same function of (s, g, h), so read_a_frag serves both.
 struct AStage256 {
   static constexpr int RA = 8;  // pieces per thread per chunk
   uint32_t oa[RA], la[RA];
+  template <bool MX8 = false>
   __device__ __attribute__((always_inline)) inline void init(const GemmArgs& g, int m0, int tid) {
 #pragma unroll
     for (int it = 0; it < RA; ++it) {
       const int q = it * 256 + tid;
       const int p = q >> 8, rr = (q >> 3) & 31, c = q & 7;
+      const int s = c >> 2, gg = MX8 ? (c & 1) : ((c >> 1) & 1), h = MX8 ? ((c >> 1) & 1) : (c & 1);
       const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
       oa[it] = (row < (uint32_t)g.m) ? row * (uint32_t)g.lda + 16u * c : 0x80000000u;
-      la[it] = (uint32_t)(p * 4096 + (2 * (c >> 2) + (c & 1)) * 1024 + (((rr + 32 * ((c >> 1) & 1)) ^ c) * 16));
+      la[it] = (uint32_t)(p * 4096 + (2 * s + h) * 1024 + (((rr + 32 * gg) ^ (4 * s + 2 * gg + 9 * h)) * 16));
     }
   }
 };
@@ -726,7 +734,7 @@ __device__ __attribute__((always_inline)) inline v8i read_a_frag(const uint8_t* 
   const int x = 4 * s + 2 * (lane >> 5);
   const uint8_t* p = st + panel * 4096 + s * 2048;
   const v4i lo = *reinterpret_cast<const v4i*>(p + ((lane ^ x) * 16));
-  const v4i hi = *reinterpret_cast<const v4i*>(p + 1024 + ((lane ^ (x + 1)) * 16));
+  const v4i hi = *reinterpret_cast<const v4i*>(p + 1024 + ((lane ^ (x + 9)) * 16));
   return (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 }
 
@@ -921,6 +929,217 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------------- MXFP8 (W8A8, MX block scaling)
+// OCP MXFP8 x MXFP8: the W8A8 kernel above with the E8M0 block scales handed
+// to the block-scaled matrix instruction. With fp8 operands that instruction
+// takes a row's 32-element scale block h from register half h of both lane
+// halves (elements 32 h + 16 g of the step in lane half g), and the scale of
+// block h from lane half h, so weights and activations are laid out that way
+// (MXFP8 packing, AStage256<MX8>):
+//   weights     : the FP8 packed images, plus one dword per panel, 256-wide
+//                 group and lane holding the lane's scales of its four steps
+//                 (the MXFP4 scale layout); chunk kc uses bytes 2 (kc % 2) + s;
+//   activations : codes staged as in the W8A8 kernel; the row's 4 scales of a
+//                 128-wide chunk staged beside them, re-ordered to
+//                 [half 0: steps 0, 1][half 1: steps 0, 1], one 16-bit read per
+//                 lane and panel.
+// K must be a multiple of 256 (whole chunk pairs, no odd first chunk); no
+// tensor scales.
+__global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
+  constexpr int A_CODES = 8 * 4096;
+  constexpr int A_STAGE = A_CODES + 256 * 4;
+  constexpr int RA = AStage256::RA;
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int OUT_STAGE = 32 * (64 * 4 + 16);
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t sout[4 * OUT_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 31, gq = lane >> 5;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const uint32_t ks = (uint32_t)(g.k >> 5);  // A scale bytes per row
+  const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
+  const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a_bscale), 0, (int)((int64_t)g.m * ks), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 4096), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_bs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * (kcn >> 1) * 256), 0x00020000);
+
+  AStage256 A;
+  uint32_t ob[4], osb[4], osa;
+  v4i ga[RA];
+  uint32_t gs;         // staged activation scales of the thread's row (4 blocks of a chunk)
+  v8i fb[2][2][4];     // [chunk parity][step][weight panel]
+  uint32_t bsc[4];     // weight scales of the current chunk pair [panel]: byte 2 (kc % 2) + s
+  uint32_t bsn[4];     // ... of the next pair
+  uint32_t asc[4];     // activation scales of the current chunk [panel]: byte s (low half)
+  v8i fa[2];
+  v16f acc[4][4];
+
+  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  auto load_a = [&](int kc) __attribute__((always_inline)) {
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int it = 0; it < RA; ++it)
+      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + kc * 128) | hi, 0, 0);
+    gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (osa + kc * 4) | hi, 0, 0);
+  };
+  // blocks 0..3 of the chunk -> [half 0: 0 2][half 1: 1 3]
+  auto write_a_scales = [&](uint8_t* st) __attribute__((always_inline)) {
+    *reinterpret_cast<uint32_t*>(st + A_CODES + tid * 4) = __builtin_amdgcn_perm(0u, gs, 0x03010200u);
+  };
+  auto write_a = [&](uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) *reinterpret_cast<v4i*>(st + A.la[it]) = ga[it];
+    write_a_scales(st);
+  };
+  auto read_asc = [&](const uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      asc[i] = *reinterpret_cast<const uint16_t*>(st + A_CODES + ((wm * 4 + i) * 32 + r) * 4 + 2 * gq);
+  };
+  auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t o = (ob[j] + kc * 4096 + s * 2048) | hi;
+        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
+        const v4i hi2 = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
+        fb[P][s][j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi2.x, hi2.y, hi2.z, hi2.w};
+      }
+  };
+  // the weight scale dwords of the chunk pair starting at chunk kc (even)
+  auto load_bs = [&](int kc) __attribute__((always_inline)) {
+    const uint32_t hi = past(kc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bsn[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + (kc >> 1) * 256) | hi, 0, 0);
+  };
+  // MFMA group f = (step f / 4, activation panel f % 4); chunk parity P
+  auto mgroup = [&](auto Pc, auto Fc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value, f = decltype(Fc)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[f & 3][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[P][f >> 2][j], fa[f & 1], acc[f & 3][j], 0, 0,
+                                                                       2 * P + (f >> 2), (int)bsc[j], f >> 2,
+                                                                       (int)asc[f & 3]);
+  };
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    // step 0: weight loads of chunk kc + 1 (and, in the first chunk of a
+    // pair, the scale dwords of the next pair), activation fragments 1..4
+    load_b(std::integral_constant<int, P ^ 1>(), kc + 1);
+    if (P == 0) load_bs(kc + 2);
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 1) & 1] = read_a_frag(cur, wm * 4 + ((F + 1) & 3), (F + 1) >> 2, lane),
+        mgroup(Pc, std::integral_constant<int, F>())), ...);
+    }(std::make_integer_sequence<int, 4>());
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (weights)
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // step 1, groups 4..6: stage activations of chunk kc + 1, load kc + 2
+    const uint32_t a_hi = past(kc + 2);
+    [&]<int... F>(std::integer_sequence<int, F...>) {
+      ((fa[(F + 5) & 1] = read_a_frag(cur, wm * 4 + ((F + 5) & 3), (F + 5) >> 2, lane),
+        [&] {
+#pragma unroll
+          for (int it = 3 * F; it < 3 * F + 3 && it < RA; ++it) *reinterpret_cast<v4i*>(nxt + A.la[it]) = ga[it];
+          if (F == 2) write_a_scales(nxt);
+        }(),
+        mgroup(Pc, std::integral_constant<int, F + 4>()),
+        [&] {
+#pragma unroll
+          for (int it = 3 * F; it < 3 * F + 3 && it < RA; ++it)
+            ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + (kc + 2) * 128) | a_hi, 0, 0);
+          if (F == 2) gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (osa + (kc + 2) * 4) | a_hi, 0, 0);
+        }()), ...);
+    }(std::make_integer_sequence<int, 3>());
+#pragma unroll
+    for (int f = 4; f < 7; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (t < 3 && 3 * (f - 4) + t < RA) {
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (activations)
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // group 7 covers the reads of the next chunk's first fragment and scales
+    fa[0] = read_a_frag(nxt, wm * 4, 0, lane);
+    mgroup(Pc, std::integral_constant<int, 7>());
+    read_asc(nxt);
+    if (P == 1) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bsc[j] = bsn[j];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 256, n0 = bn * 256;
+    A.init<true>(g, m0, tid);
+    {
+      const uint32_t row = (uint32_t)(m0 + tid);
+      osa = (row < (uint32_t)g.m) ? row * ks : OOB;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 4 + j);
+      const bool in = panel < (uint32_t)npanels_w;
+      ob[j] = in ? panel * (uint32_t)(kcn * 4096) + 16u * lane : OOB;
+      osb[j] = in ? panel * (uint32_t)((kcn >> 1) * 256) + 4u * lane : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    load_a(0);
+    write_a(smem);
+    load_bs(0);
+    __syncthreads();
+    load_a(1);
+    load_b(std::integral_constant<int, 0>(), 0);
+    fa[0] = read_a_frag(smem, wm * 4, 0, lane);
+    read_asc(smem);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bsc[j] = bsn[j];
+    for (int kc = 0; kc < kcn; kc += 2) {
+      chunk(std::integral_constant<int, 0>(), kc);
+      chunk(std::integral_constant<int, 1>(), kc + 1);
+    }
+    if (fast_out && m0 + 256 <= g.m && n0 + 256 <= g.n)
+      store_tiles_fast<4, 4>(g, acc, sout + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, 1.0f);
+    else
+      store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, 1.0f);
+  }
+}
+
 // ---------------------------------------------------------------- W4A4 (NVFP4), large token counts
 // Four E4M3 block scales (one dword, block b in byte b; never negative) to
 // fp16, exact: the E4M3 bit pattern shifted into the fp16 field is the value
@@ -1022,7 +1241,7 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   auto read_a_half = [&](const uint8_t* st, int h) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      ac[h][i] = *reinterpret_cast<const v4i*>(st + (wm * 4 + i) * 2048 + h * 1024 + ((lane ^ (h + 2 * gq)) * 16));
+      ac[h][i] = *reinterpret_cast<const v4i*>(st + (wm * 4 + i) * 2048 + h * 1024 + ((lane ^ (4 * h + 10 * gq)) * 16));
   };
   auto read_a_scales = [&](const uint8_t* st) __attribute__((always_inline)) {
 #pragma unroll
@@ -1122,7 +1341,9 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
       const int p = q >> 7, rr = (q >> 2) & 31, c = q & 3;
       const uint32_t row = (uint32_t)(m0 + 32 * p + rr);
       oa[it] = (row < (uint32_t)g.m) ? row * ka + 16u * c : OOB;
-      la[it] = (uint32_t)(p * 2048 + (c & 1) * 1024 + (((rr + 32 * (c >> 1)) ^ c) * 16));
+      // slot XOR 4 h + 10 g: the 4 pieces of a row and 2 or 4 neighbouring
+      // rows fall into distinct bank groups (checked on the CPU)
+      la[it] = (uint32_t)(p * 2048 + (c & 1) * 1024 + (((rr + 32 * (c >> 1)) ^ (4 * (c & 1) + 10 * (c >> 1))) * 16));
     }
     {
       const uint32_t row = (uint32_t)(m0 + tid);
@@ -1762,7 +1983,7 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, m, n, ldy, (int)f32out);
     return hipGetLastError();
   }
-  const int w_fmt = (a_fmt == 1) ? 1 : (a_fmt == 3) ? 3 : 2;
+  const int w_fmt = (a_fmt == 1 || a_fmt == 3 || a_fmt == 4) ? a_fmt : 2;
   GemmArgs g;
   g.a = reinterpret_cast<const uint8_t*>(a);
   g.a_bscale = a_bscale;
@@ -1779,6 +2000,13 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   g.f32out = f32out ? 1 : 0;
   g.tiles_m = g.tiles_n = 0;
   // persistent grids of 256 x 256 tiles, four waves of 128 x 128 each
+  if (a_fmt == 4) {
+    g.tiles_m = (g.m + 255) / 256;
+    g.tiles_n = (g.n + 255) / 256;
+    const int tiles = g.tiles_m * g.tiles_n;
+    hipLaunchKernelGGL(k_gemm_mxfp8_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    return hipGetLastError();
+  }
   if (a_fmt == 3) {
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;

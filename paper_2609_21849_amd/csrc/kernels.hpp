@@ -12,7 +12,7 @@
 namespace qg {
 
 // Packed weight buffer: a 256-byte header, then the codes region, then (for
-// NVFP4 and MXFP4) the block-scale region. Header fields (little endian):
+// NVFP4, MXFP4 and MXFP8) the block-scale region. Header fields (little endian):
 //   +0 u32 magic 'QGPW', +4 u32 layout version, +8 u32 format,
 //   +16 i64 n, +24 i64 k, +32 f32 tensor decode scale.
 // The weight is stored in panels of 32 rows (n rounded up to a multiple of
@@ -25,10 +25,10 @@ constexpr int64_t kPanel = 32;
 
 inline int64_t padded_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPanel; }
 inline int64_t packed_codes_bytes(int fmt, int64_t n, int64_t k) {
-  return fmt == 1 ? padded_rows(n) * k : padded_rows(n) * k / 2;
+  return (fmt == 1 || fmt == 4) ? padded_rows(n) * k : padded_rows(n) * k / 2;
 }
 inline int64_t packed_scale_bytes(int fmt, int64_t n, int64_t k) {
-  return fmt == 2 ? padded_rows(n) * k / 16 : fmt == 3 ? padded_rows(n) * k / 32 : 0;
+  return fmt == 2 ? padded_rows(n) * k / 16 : (fmt == 3 || fmt == 4) ? padded_rows(n) * k / 32 : 0;
 }
 inline int64_t packed_total_bytes(int fmt, int64_t n, int64_t k) {
   return kPackHeader + packed_codes_bytes(fmt, n, k) + packed_scale_bytes(fmt, n, k);

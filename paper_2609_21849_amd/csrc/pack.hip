@@ -20,9 +20,15 @@
 //          E8M0 scales in their own region, per 256-wide chunk c one run of
 //          4 bytes per lane = the scales of the lane's blocks in steps
 //          4c .. 4c + 3 (blocks 8c + 2s + g), read as one dword per lane.
+//   MXFP8: 2048-byte step images like FP8, but lane half g and register
+//          half h hold elements 64 t + 32 h + 16 g .. + 15: the block-scaled
+//          fp8 instruction reads scale block h of a row from register half h
+//          of both lane halves (its fp8 reduction order), so each of the
+//          row's two 32-element scale blocks of the step must sit there; the
+//          MXFP4 scale region (lane half g carries the scale of block 2 t + g).
 // Chunks of one panel follow each other along k, so a panel is one
 // contiguous stream. The header keeps format, n, k and the tensor scale
-// (1.0 for MXFP4, which has none).
+// (1.0 for the MX formats, which have none).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -55,13 +61,14 @@ __device__ inline int64_t canon_piece(int fmt, int64_t p, int64_t n, int64_t k) 
     return row * (k / 2) + t * 32 + 16 * (l >> 5);
   }
   const int64_t kc_n = k / 128;
-  const int per = (fmt == 1) ? 256 : 128;            // pieces per chunk
+  const int per = (fmt == 1 || fmt == 4) ? 256 : 128;  // pieces per chunk
   const int64_t chunk = p / per, s = p - chunk * per;
   const int64_t panel = chunk / kc_n, kc = chunk - panel * kc_n;
   const int64_t h = s >> 6, l = s & 63;
   const int64_t row = panel * 32 + (l & 31);
   if (row >= n) return -1;
   if (fmt == 1) return row * k + kc * 128 + 64 * (h >> 1) + 32 * (l >> 5) + 16 * (h & 1);
+  if (fmt == 4) return row * k + kc * 128 + 64 * (h >> 1) + 32 * (h & 1) + 16 * (l >> 5);
   return row * (k / 2) + kc * 64 + 32 * (l >> 5) + 16 * h;
 }
 
@@ -136,7 +143,7 @@ hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, con
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<true>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt,
                      const_cast<uint8_t*>(codes), pc, npieces, n, k);
-  if (fmt == 3) {
+  if (fmt == 3 || fmt == 4) {
     const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_mx_scales<true>, dim3(blocks_for(nruns)), dim3(256), 0, st,
                        const_cast<uint8_t*>(bscale), pc + cb, nruns, n, k);
@@ -158,7 +165,7 @@ hipError_t launch_unpack(int fmt, const uint8_t* packed, int64_t n, int64_t k, u
   const int64_t npieces = cb / 16;
   hipLaunchKernelGGL(k_pack_codes<false>, dim3(blocks_for(npieces)), dim3(256), 0, st, fmt, codes,
                      pc, npieces, n, k);
-  if (fmt == 3) {
+  if (fmt == 3 || fmt == 4) {
     const int64_t nruns = padded_rows(n) * k / 128;
     hipLaunchKernelGGL(k_pack_mx_scales<false>, dim3(blocks_for(nruns)), dim3(256), 0, st, bscale,
                        pc + cb, nruns, n, k);

@@ -166,7 +166,8 @@ def test_mx_packed_bytes():
     assert q.qg_packed_bytes(MXFP4, 64, 256) == 256 + 64 * 256 // 2 + 64 * 256 // 32
     assert q.qg_packed_bytes(MXFP4, 48, 512) == 256 + 64 * 512 // 2 + 64 * 512 // 32   # 32-row panels
     assert q.qg_packed_bytes(MXFP4, 64, 128) == 0     # MXFP4 weights need k % 256
-    assert q.qg_packed_bytes(MXFP8, 64, 256) == 0     # MXFP8 weights are not packable
+    assert q.qg_packed_bytes(MXFP8, 64, 256) == 256 + 64 * 256 + 64 * 256 // 32
+    assert q.qg_packed_bytes(MXFP8, 64, 384) == 0     # MX weights need k % 256
 
 
 def test_mx_quantize_validation():
@@ -185,7 +186,8 @@ def test_mx_quantize_validation():
 
 @pytest.mark.parametrize("unpack", [False, True])
 def test_mx_pack_validation(unpack):
-    assert _pack(MXFP8, ts=None, k=256, unpack=unpack) == UNSUP
+    assert _pack(MXFP8, ts=None, k=384, unpack=unpack) == SHAPE       # k % 256
+    assert _pack(MXFP8, k=256, unpack=unpack) == INVALID              # no tensor scale
     assert _pack(MXFP4, ts=None, k=128, unpack=unpack) == SHAPE       # k % 256
     assert _pack(MXFP4, ts=None, n=24, k=256, unpack=unpack) == SHAPE
     assert _pack(MXFP4, k=256, unpack=unpack) == INVALID              # no tensor scale
@@ -197,7 +199,11 @@ def test_mx_gemm_validation():
     mx = dict(a_fmt=MXFP4, w_fmt=MXFP4, ats=None)
     assert _gemm(a_fmt=MXFP4, w_fmt=NVFP4, ats=None) == UNSUP
     assert _gemm(a_fmt=NVFP4, w_fmt=MXFP4) == UNSUP
-    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8, ats=None) == UNSUP
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP4, ats=None) == UNSUP
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8, ats=None, k=384, lda=384) == SHAPE
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8) == INVALID                 # no tensor scale
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8, ats=None, abs_=P + 2) == INVALID   # 4-byte aligned scales
+    assert _gemm(a_fmt=MXFP8, w_fmt=MXFP8, ats=None, lda=512) == INVALID      # dense codes
     assert _gemm(a_fmt=BF16, w_fmt=MXFP4, abs_=None, ats=None) == UNSUP
     assert _gemm(**mx, k=384, lda=384) == SHAPE                       # k % 256
     assert _gemm(a_fmt=MXFP4, w_fmt=MXFP4) == INVALID                 # MX A has no tensor scale

@@ -1,6 +1,6 @@
-"""GPU parity of the OCP MX path (MXFP4 / MXFP8 quantizer and dequantizer,
-MXFP4 weight packing, the MXFP4 x MXFP4 GEMM on the block-scaled matrix
-instruction) with the CPU oracle: codes and E8M0 scales bit-exact, decoded
+"""GPU parity of the OCP MX path (MXFP4 / MXFP8 quantizer, dequantizer and
+weight packing, the MXFP4 x MXFP4 and MXFP8 x MXFP8 GEMMs on the block-scaled
+matrix instruction) with the CPU oracle: codes and E8M0 scales bit-exact, decoded
 values bit-exact, GEMM outputs within |y - y_ref| <= 1e-3 * sum_k |a w| of the
 oracle's fp64 product over the same quantized operands."""
 import numpy as np
@@ -116,12 +116,13 @@ def test_mx_dequant_bit_exact(fmt, out):
         assert np.array_equal(host(d.view(torch.int16)).view(np.uint16), want)
 
 
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
 @pytest.mark.parametrize("n,k", [(16, 256), (48, 512), (80, 768), (3072, 3072)])
-def test_mxfp4_pack_unpack_roundtrip(n, k):
+def test_mx_pack_unpack_roundtrip(fmt, n, k):
     w = synth.normal_bf16(n, k, 0.02, 9, 1)
-    wq = q.quantize(to_dev_bf16(w), MXFP4)
+    wq = q.quantize(to_dev_bf16(w), fmt)
     packed = q.pack(wq)
-    back = q.unpack(packed, MXFP4, n, k)
+    back = q.unpack(packed, fmt, n, k)
     torch.cuda.synchronize()
     assert torch.equal(back.codes, wq.codes)
     assert torch.equal(back.block_scales, wq.block_scales)
@@ -134,12 +135,12 @@ def test_mxfp4_pack_unpack_roundtrip(n, k):
     assert np.array_equal(np.sort(body), np.sort(expect))
 
 
-def run_mx_linear(x, w, out=q.QG_OUT_BF16, check_codes=True):
+def run_mx_linear(x, w, out=q.QG_OUT_BF16, check_codes=True, fmt=MXFP4):
     xd, wd = to_dev_bf16(x), to_dev_bf16(w)
-    wq = q.quantize(wd, MXFP4)
+    wq = q.quantize(wd, fmt)
     packed = q.pack(wq)
-    a = q.quantize(xd, MXFP4)
-    y = q.linear(a, packed, MXFP4, w.shape[0], out_dtype=out)
+    a = q.quantize(xd, fmt)
+    y = q.linear(a, packed, fmt, w.shape[0], out_dtype=out)
     torch.cuda.synchronize()
     if check_codes:
         assert_mx_equal(wq, w)
@@ -150,15 +151,17 @@ def run_mx_linear(x, w, out=q.QG_OUT_BF16, check_codes=True):
 @pytest.mark.parametrize("m,n,k", [(1, 16, 256), (17, 48, 256), (64, 256, 512), (300, 272, 768),
                                    (257, 512, 1024), (512, 768, 1280), (100, 2080, 512), (129, 528, 2304)])
 @pytest.mark.parametrize("out", [q.QG_OUT_F32, q.QG_OUT_BF16])
-def test_mxfp4_gemm_small_full_parity(m, n, k, out):
-    log("mxfp4 gemm m=%d n=%d k=%d out=%d" % (m, n, k, out))
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
+def test_mx_gemm_small_full_parity(fmt, m, n, k, out):
+    log("%s gemm m=%d n=%d k=%d out=%d" % (NAME[fmt], m, n, k, out))
     x = synth.normal_bf16(m, k, 1.0, 11, 0)
     w = synth.normal_bf16(n, k, 0.02, 11, 1)
-    y = run_mx_linear(x, w, out)
-    log("  max err/B", check_linear(y, oracle.linear_reference("mxfp4", x, w)))
+    y = run_mx_linear(x, w, out, fmt=fmt)
+    log("  max err/B", check_linear(y, oracle.linear_reference(NAME[fmt], x, w)))
 
 
-def test_mxfp4_gemm_zero_rows_and_blocks():
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
+def test_mx_gemm_zero_rows_and_blocks(fmt):
     # an all-zero activation row gives an exactly zero output row; zero blocks
     # (E8M0 code 0) elsewhere contribute nothing
     m, n, k = 40, 64, 512
@@ -167,20 +170,21 @@ def test_mxfp4_gemm_zero_rows_and_blocks():
     x[7, 64:160] = 0
     w = synth.normal_bf16(n, k, 0.02, 12, 1)
     w[3, :256] = 0
-    y = run_mx_linear(x, w, q.QG_OUT_F32)
+    y = run_mx_linear(x, w, q.QG_OUT_F32, fmt=fmt)
     assert not torch.any(y[5]).item()
-    check_linear(y, oracle.linear_reference("mxfp4", x, w))
+    check_linear(y, oracle.linear_reference(NAME[fmt], x, w))
 
 
-def test_mxfp4_gemm_row_independent_of_batch():
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
+def test_mx_gemm_row_independent_of_batch(fmt):
     # the same activation row gives bit-identical outputs whatever the batch
     n, k = 512, 1024
     x = synth.normal_bf16(600, k, 1.0, 13, 0)
     w = synth.normal_bf16(n, k, 0.02, 13, 1)
-    y_all = run_mx_linear(x, w, q.QG_OUT_F32, check_codes=False)
-    y_one = run_mx_linear(x[299:300], w, q.QG_OUT_F32, check_codes=False)
+    y_all = run_mx_linear(x, w, q.QG_OUT_F32, check_codes=False, fmt=fmt)
+    y_one = run_mx_linear(x[299:300], w, q.QG_OUT_F32, check_codes=False, fmt=fmt)
     assert torch.equal(y_all[299:300], y_one)
-    y_again = run_mx_linear(x, w, q.QG_OUT_F32, check_codes=False)
+    y_again = run_mx_linear(x, w, q.QG_OUT_F32, check_codes=False, fmt=fmt)
     assert torch.equal(y_all, y_again)
 
 
@@ -191,14 +195,15 @@ def _sample(m, n, count, seed):
     return rows, cols
 
 
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
 @pytest.mark.parametrize("name", list(synth.DIT_LINEARS))
-def test_mxfp4_dit_linear_sampled(name):
+def test_mx_dit_linear_sampled(fmt, name):
     n, k = synth.DIT_LINEARS[name]
     m = synth.DIT_TOKENS
-    log("dit mxfp4 %s m=%d n=%d k=%d" % (name, m, n, k))
+    log("dit %s %s m=%d n=%d k=%d" % (NAME[fmt], name, m, n, k))
     x = synth.normal_bf16(m, k, 1.0, 0, 0, outlier_frac=0.001, outlier_gain=50.0)
     w = synth.normal_bf16(n, k, 0.02, 0, 1)
-    y = run_mx_linear(x, w)
+    y = run_mx_linear(x, w, fmt=fmt)
     rows, cols = _sample(m, n, 3000, 1)
-    ref = oracle.linear_reference("mxfp4", x, w, rows=rows, cols=cols)
+    ref = oracle.linear_reference(NAME[fmt], x, w, rows=rows, cols=cols)
     log("  max err/B", check_linear(y, ref, rows, cols))

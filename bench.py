@@ -224,7 +224,8 @@ def main():
             ent["a_" + kind] = q.QTensor(fmt, codes, bs, torch.empty(1, device="cuda"), M, k)
             ent["y_" + kind] = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
         ent["w_bf16"] = wd  # for the BF16 baseline of the block chain
-        ent["w_mxfp4"] = q.pack(q.quantize(wd, q.QG_FMT_MXFP4))  # the hardware-native 4-bit variant
+        ent["w_mxfp4"] = q.pack(q.quantize(wd, q.QG_FMT_MXFP4))  # the hardware-native block-scaled formats
+        ent["w_mxfp8"] = q.pack(q.quantize(wd, q.QG_FMT_MXFP8))
         dit.append(ent)
     enc = []
     for ei, (name, (n, k)) in enumerate(synth.ENCODER_LINEARS.items()):
@@ -331,7 +332,7 @@ def main():
     parts["w4a16_single_call"] = w4
     parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
     parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
-    parts["mxfp4"] = mxfp4_part(q, lib, st, dit, M, flops, parts["nvfp4"])
+    parts["mx"] = mx_part(q, lib, st, dit, M, flops, parts["nvfp4"], parts["fp8"])
     parts["dit_block_chain"] = block_chain_part(q, dit, M)
     parts["weight_streaming"] = weight_streaming_part(q, dit, M)
     parts["w8a8_encoder"] = w8a8_encoder_part(q, enc)
@@ -440,7 +441,8 @@ def block_chain_part(q, dit, M, steps=10):
 
     runs = {"bf16": chain_bf16, "fp8": lambda: chain_q("fp8", q.QG_FMT_FP8_E4M3),
             "nvfp4": lambda: chain_q("nvfp4", q.QG_FMT_NVFP4),
-            "mxfp4": lambda: chain_q("mxfp4", q.QG_FMT_MXFP4)}
+            "mxfp4": lambda: chain_q("mxfp4", q.QG_FMT_MXFP4),
+            "mxfp8": lambda: chain_q("mxfp8", q.QG_FMT_MXFP8)}
     res = {}
     outs = {}
     for name, fn in runs.items():
@@ -454,7 +456,7 @@ def block_chain_part(q, dit, M, steps=10):
         s1.record()
         torch.cuda.synchronize()
         res[name] = {"ms": round(s0.elapsed_time(s1) / steps, 4)}
-    for name in ("fp8", "nvfp4", "mxfp4"):
+    for name in ("fp8", "nvfp4", "mxfp4", "mxfp8"):
         res[name]["speedup_vs_bf16"] = round(res["bf16"]["ms"] / res[name]["ms"], 3)
         # agreement of the chain output with the BF16 chain (relative Frobenius error)
         d = (outs[name].float() - outs["bf16"].float()).norm() / outs["bf16"].float().norm()
@@ -464,65 +466,74 @@ def block_chain_part(q, dit, M, steps=10):
     return res
 
 
-def mxfp4_part(q, lib, st, dit, M, flops, nvfp4, steps=10):
-    """The DiT linears in OCP MXFP4 (E2M1, E8M0 scale per 32, no tensor
-    scale): one quantize kernel + the GEMM on the block-scaled fp4 matrix
-    instruction per linear, on the same heavy-tailed activations as the NVFP4
-    step. Reports the GEMM rate against the fp4 peak, the speed-up over the
-    exact NVFP4 GEMM, and how far each 4-bit format's output lies from the
+def mx_part(q, lib, st, dit, M, flops, nvfp4, fp8, steps=10):
+    """The DiT linears in the OCP MX formats (E2M1 / E4M3 elements, E8M0
+    scale per 32, no tensor scale): one quantize kernel + the GEMM on the
+    block-scaled matrix instruction per linear, on the same heavy-tailed
+    activations as the NVFP4 step. Reports the GEMM rate against the format's
+    peak, the speed-up over the exact NVFP4 GEMM (MXFP4) and the per-tensor
+    FP8 GEMM (MXFP8), and how far each format's output lies from the
     unquantized product (relative Frobenius error against torch.mm in fp32
     of the bf16 operands, sampled rows)."""
     import torch
-    plan, bufs = [], {}
-    for e in dit:
-        k, n = e["k"], e["n"]
-        codes = torch.empty((M, k // 2), dtype=torch.uint8, device="cuda")
-        bs = torch.empty((M, k // 32), dtype=torch.uint8, device="cuda")
-        y = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
-        bufs[e["name"]] = (codes, bs, y)
-        plan.append((("mxquant", e["name"]), lib.qg_quantize_act,
-                     (q.QG_FMT_MXFP4, e["x"]["nvfp4"].data_ptr(), M, k, k, codes.data_ptr(), bs.data_ptr(), None, st)))
-        plan.append((("mxgemm", e["name"]), lib.qg_gemm,
-                     (q.QG_FMT_MXFP4, codes.data_ptr(), bs.data_ptr(), None, k, q.QG_FMT_MXFP4,
-                      e["w_mxfp4"].data_ptr(), e["w_mxfp4"].numel(), M, n, k, y.data_ptr(), n, q.QG_OUT_BF16, st)))
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plan]
-           for _ in range(steps + 2)]
-    for i in range(steps + 2):
-        for (key, fn, fargs), (s0, s1) in zip(plan, evs[i]):
-            s0.record()
-            rc = fn(*fargs)
-            s1.record()
-            if rc != 0:
-                raise q.QGError(rc, str(key))
-    torch.cuda.synchronize()
-    dur = {}
-    for i in range(2, steps + 2):
-        for (key, _, _), (s0, s1) in zip(plan, evs[i]):
-            dur.setdefault(key, []).append(s0.elapsed_time(s1))
-    gms = {e["name"]: float(np.mean(dur[("mxgemm", e["name"])])) for e in dit}
-    qms = {e["name"]: float(np.mean(dur[("mxquant", e["name"])])) for e in dit}
-    f = sum(flops(e) for e in dit)
-    g_all, q_all = sum(gms.values()), sum(qms.values())
-    rate = f / (g_all * 1e9)
-    nv_rate = nvfp4["gemm_tflops"]
-    # numerics: 4-bit outputs against the unquantized product on 256 sampled rows
-    rel = {"mxfp4": {}, "nvfp4": {}}
+    out = {}
     rows = torch.arange(0, M, M // 256, device="cuda")[:256]
+    refs = {}
     for e in dit:
-        xs = e["x"]["nvfp4"][rows].float()
-        ref = torch.mm(xs, e["w_bf16"].float().t())
-        for kind, y in (("mxfp4", bufs[e["name"]][2]), ("nvfp4", e["y_nvfp4"])):
-            rel[kind][e["name"]] = round(float((y[rows].float() - ref).norm() / ref.norm()), 4)
-    return {"per_linear": {e["name"]: {"gemm_us": round(1e3 * gms[e["name"]], 2),
-                                       "quant_us": round(1e3 * qms[e["name"]], 2),
-                                       "gemm_tflops": round(flops(e) / (gms[e["name"]] * 1e9), 1)} for e in dit},
-            "gemm_tflops": round(rate, 1),
-            "gemm_frac_of_fp4_peak": round(rate / PEAK["fp4"], 4),
-            "linear_tflops_incl_quant": round(f / ((g_all + q_all) * 1e9), 1),
-            "gemm_speedup_vs_nvfp4": round(rate / nv_rate, 3),
-            "rel_err_vs_unquantized": rel,
-            "note": "MXFP4 is the matrix-core-native 4-bit format (power-of-two scales per 32); its "
-                    "outputs differ from NVFP4's by design and are checked against their own oracle"}
+        refs[e["name"]] = torch.mm(e["x"]["nvfp4"][rows].float(), e["w_bf16"].float().t())
+    for kind, fmt in (("mxfp4", q.QG_FMT_MXFP4), ("mxfp8", q.QG_FMT_MXFP8)):
+        plan, bufs = [], {}
+        for e in dit:
+            k, n = e["k"], e["n"]
+            codes = torch.empty((M, k // 2 if kind == "mxfp4" else k), dtype=torch.uint8, device="cuda")
+            bs = torch.empty((M, k // 32), dtype=torch.uint8, device="cuda")
+            y = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
+            bufs[e["name"]] = (codes, bs, y)
+            plan.append((("mxquant", e["name"]), lib.qg_quantize_act,
+                         (fmt, e["x"]["nvfp4"].data_ptr(), M, k, k, codes.data_ptr(), bs.data_ptr(), None, st)))
+            plan.append((("mxgemm", e["name"]), lib.qg_gemm,
+                         (fmt, codes.data_ptr(), bs.data_ptr(), None, k, fmt, e["w_" + kind].data_ptr(),
+                          e["w_" + kind].numel(), M, n, k, y.data_ptr(), n, q.QG_OUT_BF16, st)))
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plan]
+               for _ in range(steps + 2)]
+        for i in range(steps + 2):
+            for (key, fn, fargs), (s0, s1) in zip(plan, evs[i]):
+                s0.record()
+                rc = fn(*fargs)
+                s1.record()
+                if rc != 0:
+                    raise q.QGError(rc, str(key))
+        torch.cuda.synchronize()
+        dur = {}
+        for i in range(2, steps + 2):
+            for (key, _, _), (s0, s1) in zip(plan, evs[i]):
+                dur.setdefault(key, []).append(s0.elapsed_time(s1))
+        gms = {e["name"]: float(np.mean(dur[("mxgemm", e["name"])])) for e in dit}
+        qms = {e["name"]: float(np.mean(dur[("mxquant", e["name"])])) for e in dit}
+        f = sum(flops(e) for e in dit)
+        g_all, q_all = sum(gms.values()), sum(qms.values())
+        rate = f / (g_all * 1e9)
+        rel = {e["name"]: round(float((bufs[e["name"]][2][rows].float() - refs[e["name"]]).norm()
+                                      / refs[e["name"]].norm()), 4) for e in dit}
+        out[kind] = {"per_linear": {e["name"]: {"gemm_us": round(1e3 * gms[e["name"]], 2),
+                                                "quant_us": round(1e3 * qms[e["name"]], 2),
+                                                "gemm_tflops": round(flops(e) / (gms[e["name"]] * 1e9), 1)}
+                                    for e in dit},
+                     "gemm_tflops": round(rate, 1),
+                     "gemm_frac_of_%s_peak" % ("fp4" if kind == "mxfp4" else "fp8"):
+                         round(rate / PEAK["fp4" if kind == "mxfp4" else "fp8"], 4),
+                     "linear_tflops_incl_quant": round(f / ((g_all + q_all) * 1e9), 1),
+                     "rel_err_vs_unquantized": rel}
+        if kind == "mxfp4":
+            out[kind]["gemm_speedup_vs_nvfp4"] = round(rate / nvfp4["gemm_tflops"], 3)
+        else:
+            out[kind]["gemm_speedup_vs_fp8"] = round(rate / fp8["gemm_tflops"], 3)
+    out["nvfp4_rel_err_vs_unquantized"] = {
+        e["name"]: round(float((e["y_nvfp4"][rows].float() - refs[e["name"]]).norm() / refs[e["name"]].norm()), 4)
+        for e in dit}
+    out["note"] = ("MX formats are the matrix-core-native block scaling (power-of-two scales per 32); their "
+                   "outputs differ from NVFP4's / FP8's by design and are checked against their own oracle")
+    return out
 
 
 def weight_streaming_part(q, dit, M, blocks=8, steps=3):

@@ -439,7 +439,42 @@ def block_chain_part(q, dit, M, steps=10):
         u = F.gelu(lin(a, "mlp_up"), approximate="tanh")
         return lin(u, "mlp_down")
 
+    # FP8 with static (calibrated) activation scales and the quantization of
+    # QKV's and attention-out's outputs fused into their GEMM epilogues
+    # (qg_gemm_quant); the scales are those the dynamic chain derives
+    FP8 = q.QG_FMT_FP8_E4M3
+
+    def calibrate():
+        sc = {}
+        a0 = q.quantize(x0, FP8)
+        h = q.linear(a0, by["qkv"]["w_fp8"], FP8, 9216)
+        av = q.quantize(h[:, 6144:9216], FP8)
+        a = q.linear(av, by["attn_out"]["w_fp8"], FP8, 3072)
+        aa = q.quantize(a, FP8)
+        u = F.gelu(q.linear(aa, by["mlp_up"]["w_fp8"], FP8, 9216), approximate="tanh")
+        au = q.quantize(u, FP8)
+        for key, t in (("x0", a0), ("v", av), ("a", aa), ("u", au)):
+            sc[key] = t.tensor_scale.clone()
+        return sc
+
+    cal = calibrate()
+    qkv_codes = torch.empty((M, 9216), dtype=torch.uint8, device="cuda")
+    ao_codes = torch.empty((M, 3072), dtype=torch.uint8, device="cuda")
+
+    def chain_fp8_fused():
+        a0 = q.quantize(x0, FP8, static_scale=cal["x0"])
+        wq, wa = by["qkv"]["w_fp8"], by["attn_out"]["w_fp8"]
+        q.qg_gemm_quant(FP8, a0.codes, None, a0.tensor_scale, 3072, FP8, wq, wq.numel(), M, 9216, 3072,
+                        qkv_codes, 9216, cal["v"])
+        # the V third of the QKV codes is the attention-out operand (row pitch 9216)
+        q.qg_gemm_quant(FP8, qkv_codes.data_ptr() + 6144, None, cal["v"], 9216, FP8, wa, wa.numel(), M, 3072,
+                        3072, ao_codes, 3072, cal["a"])
+        u = F.gelu(q.linear(q.QTensor(FP8, ao_codes, None, cal["a"], M, 3072), by["mlp_up"]["w_fp8"], FP8, 9216),
+                   approximate="tanh")
+        return q.linear(q.quantize(u, FP8, static_scale=cal["u"]), by["mlp_down"]["w_fp8"], FP8, 3072)
+
     runs = {"bf16": chain_bf16, "fp8": lambda: chain_q("fp8", q.QG_FMT_FP8_E4M3),
+            "fp8_static_fused": chain_fp8_fused,
             "nvfp4": lambda: chain_q("nvfp4", q.QG_FMT_NVFP4),
             "mxfp4": lambda: chain_q("mxfp4", q.QG_FMT_MXFP4),
             "mxfp8": lambda: chain_q("mxfp8", q.QG_FMT_MXFP8)}
@@ -456,13 +491,16 @@ def block_chain_part(q, dit, M, steps=10):
         s1.record()
         torch.cuda.synchronize()
         res[name] = {"ms": round(s0.elapsed_time(s1) / steps, 4)}
-    for name in ("fp8", "nvfp4", "mxfp4", "mxfp8"):
+    for name in ("fp8", "fp8_static_fused", "nvfp4", "mxfp4", "mxfp8"):
         res[name]["speedup_vs_bf16"] = round(res["bf16"]["ms"] / res[name]["ms"], 3)
         # agreement of the chain output with the BF16 chain (relative Frobenius error)
         d = (outs[name].float() - outs["bf16"].float()).norm() / outs["bf16"].float().norm()
         res[name]["rel_err_vs_bf16"] = round(float(d), 4)
+    d = (outs["fp8_static_fused"].float() - outs["fp8"].float()).norm() / outs["fp8"].float().norm()
+    res["fp8_static_fused"]["rel_diff_vs_fp8_chain"] = round(float(d), 4)
     res["note"] = ("chain time includes the activation quantizers, GELU and the allocating Python "
-                   "helpers; attention is stubbed")
+                   "helpers; attention is stubbed; fp8_static_fused: calibrated activation scales, the QKV "
+                   "and attention-out outputs quantized in their GEMM epilogues (qg_gemm_quant)")
     return res
 
 

@@ -215,6 +215,30 @@ qg_status qg_gemm(qg_format a_fmt, const void *a, const void *a_block_scales,
                   void *y, int64_t ldy, qg_out_dtype y_dtype, void *stream);
 
 /*
+ * qg_gemm_quant -- qg_gemm whose epilogue writes the output already
+ * quantized to FP8 E4M3 with a static (calibrated) decode scale: the next
+ * linear's activation operand, produced without the bf16 round trip through
+ * memory and without a separate quantize kernel. Paper: Sec. 4, quantization
+ * paragraph (activations quantized for the low-precision linears; PTQ with
+ * calibrated ranges).
+ *   a_fmt ... k   as for qg_gemm (every supported pair).
+ *   y_codes       out: [m, ldy] E4M3 bytes (ldy >= n, any alignment).
+ *   y_scale       in: device fp32 decode scale s_y of the output, 0 or a
+ *                 normal positive number (e.g. the scale qg_quantize_act
+ *                 derived for calibration data); not written.
+ * Result: y_codes[i,j] = E4M3(fl(y[i,j] * r)) with r = s_y > 0 ? fl(1/s_y) : 0
+ * and y[i,j] the fp32 value qg_gemm would round to its output type; E4M3()
+ * rounds to nearest even and saturates at +-448, as in qg_quantize_act. With
+ * the accuracy contract of qg_gemm, every code is a correct rounding of some
+ * value within that contract's error of the exact product.
+ */
+qg_status qg_gemm_quant(qg_format a_fmt, const void *a, const void *a_block_scales,
+                        const float *a_tensor_scale, int64_t lda,
+                        qg_format w_fmt, const void *w_packed, size_t w_packed_bytes,
+                        int64_t m, int64_t n, int64_t k,
+                        void *y_codes, int64_t ldy, const float *y_scale, void *stream);
+
+/*
  * qg_dequant -- decode a quantized tensor to bf16 or fp32.
  *   FP8  : out = fl(e4m3(q) * s)
  *   NVFP4: out = fl(fl(e2m1(q) * e4m3(s_b)) * s_t)   (the inner product is exact)

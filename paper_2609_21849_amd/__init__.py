@@ -25,7 +25,7 @@ QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
                 4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
 EXPORTS = ["qg_quantize_act", "qg_quantize_act_static", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
-           "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
+           "qg_gemm_quant", "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
            "qg_last_hip_error", "qg_abi_version"]
 
 
@@ -68,6 +68,8 @@ def lib() -> ctypes.CDLL:
         L.qg_unpack_weights.argtypes = [I32, P, SZ, I64, I64, P, P, P, P]
         L.qg_gemm.restype = I32
         L.qg_gemm.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, I32, P]
+        L.qg_gemm_quant.restype = I32
+        L.qg_gemm_quant.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, P, P]
         L.qg_dequant.restype = I32
         L.qg_dequant.argtypes = [I32, P, P, P, I64, I64, P, I32, P]
         D, U8 = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_uint8)
@@ -151,6 +153,34 @@ def qg_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_pa
     if check:
         _check(s, "qg_gemm")
     return s
+
+
+def qg_gemm_quant(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_packed_bytes, m, n, k,
+                  y_codes, ldy, y_scale, stream=None, check=True):
+    s = lib().qg_gemm_quant(a_fmt, _p(a), _p(a_block_scales), _p(a_tensor_scale), lda, w_fmt, _p(w_packed),
+                            w_packed_bytes, m, n, k, _p(y_codes), ldy, _p(y_scale), _stream(stream))
+    if check:
+        _check(s, "qg_gemm_quant")
+    return s
+
+
+def linear_fp8_out(a, w_packed, w_fmt: int, n: int, y_scale, stream=None) -> "QTensor":
+    """Y = A . W^T written as FP8 E4M3 codes with the static decode scale
+    y_scale (a one-element fp32 CUDA tensor): the next linear's activation."""
+    import torch
+    if isinstance(a, QTensor):
+        m, k, a_fmt = a.rows, a.cols, a.fmt
+        a_data, a_bs, a_ts, lda = a.codes, a.block_scales, a.tensor_scale, a.cols
+        dev = a.codes.device
+    else:
+        m, k = a.shape
+        a_fmt, a_data, a_bs, a_ts = QG_FMT_BF16, a, None, None
+        lda = a.stride(0) if m > 1 else k
+        dev = a.device
+    codes = torch.empty((m, n), dtype=torch.uint8, device=dev)
+    qg_gemm_quant(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, codes, n, y_scale,
+                  stream)
+    return QTensor(QG_FMT_FP8_E4M3, codes, None, y_scale, m, n)
 
 
 def _doubles(v):

@@ -67,9 +67,9 @@ qg_status check_quantize(qg_format fmt, const void* x, int64_t rows, int64_t col
 
 qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales, const float* a_tensor_scale,
                      int64_t lda, qg_format w_fmt, const void* w_packed, size_t w_packed_bytes, int64_t m,
-                     int64_t n, int64_t k, const void* y, int64_t ldy, qg_out_dtype y_dtype) {
+                     int64_t n, int64_t k, const void* y, int64_t ldy, int y_esz) {
   if (!valid_fmt(a_fmt) || !valid_fmt(w_fmt)) return QG_ERR_INVALID_ARG;
-  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+  if (y_esz != 1 && y_esz != 2 && y_esz != 4) return QG_ERR_INVALID_ARG;
   const bool w8a8 = (a_fmt == QG_FMT_FP8_E4M3 && w_fmt == QG_FMT_FP8_E4M3);
   const bool w4a4 = (a_fmt == QG_FMT_NVFP4 && w_fmt == QG_FMT_NVFP4);
   const bool w4a16 = (a_fmt == QG_FMT_BF16 && w_fmt == QG_FMT_NVFP4);
@@ -92,7 +92,7 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   }
   if (packed_total_bytes((int)w_fmt, n, k) > kMaxDim) return QG_ERR_SHAPE;
   if (m > 0 && n > 0) {
-    if (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2)) return QG_ERR_INVALID_ARG;
+    if (y == nullptr || !aligned(y, (uintptr_t)y_esz)) return QG_ERR_INVALID_ARG;
     if (k > 0) {
       if (a == nullptr) return QG_ERR_INVALID_ARG;
       if (w8a8 && (!aligned(a, 16) || lda % 16 != 0 || a_tensor_scale == nullptr || a_block_scales != nullptr))
@@ -219,13 +219,26 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
                   const float* a_tensor_scale, int64_t lda, qg_format w_fmt, const void* w_packed,
                   size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y, int64_t ldy,
                   qg_out_dtype y_dtype, void* stream) {
+  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
   const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
-                                     w_packed_bytes, m, n, k, y, ldy, y_dtype);
+                                     w_packed_bytes, m, n, k, y, ldy, y_dtype == QG_OUT_F32 ? 4 : 2);
   if (c != QG_OK) return c;
   return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
                                     a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
-                                    n, k, y, ldy, y_dtype == QG_OUT_F32,
+                                    n, k, y, ldy, y_dtype == QG_OUT_F32 ? 1 : 0, nullptr,
                                     reinterpret_cast<hipStream_t>(stream)));
+}
+
+qg_status qg_gemm_quant(qg_format a_fmt, const void* a, const void* a_block_scales, const float* a_tensor_scale,
+                        int64_t lda, qg_format w_fmt, const void* w_packed, size_t w_packed_bytes, int64_t m,
+                        int64_t n, int64_t k, void* y_codes, int64_t ldy, const float* y_scale, void* stream) {
+  if (y_scale == nullptr || !aligned(y_scale, 4)) return QG_ERR_INVALID_ARG;
+  const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
+                                     w_packed_bytes, m, n, k, y_codes, ldy, 1);
+  if (c != QG_OK) return c;
+  return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
+                                    a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
+                                    n, k, y_codes, ldy, 2, y_scale, reinterpret_cast<hipStream_t>(stream)));
 }
 
 qg_status qg_dequant(qg_format fmt, const void* codes, const void* block_scales,

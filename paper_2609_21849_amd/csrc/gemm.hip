@@ -63,9 +63,50 @@ struct GemmArgs {
   int m, n, k;
   void* y;
   int64_t ldy;
-  int f32out;
+  int out_mode;             // OUT_BF16, OUT_F32 or OUT_FP8 (E4M3 codes, static scale)
+  const float* y_scale;     // decode scale of the FP8 output
   int tiles_m, tiles_n;
 };
+
+constexpr int OUT_BF16 = 0, OUT_F32 = 1, OUT_FP8 = 2;
+
+// Reciprocal of the FP8 output's decode scale (the static quantizer's r).
+__device__ __attribute__((always_inline)) inline float out_rscale(const GemmArgs& g) {
+  if (g.out_mode != OUT_FP8) return 0.0f;
+  const float s = *g.y_scale;
+  return (s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
+}
+
+// Four consecutive outputs y[m][n .. n+3] (n % 4 == 0) in the output format:
+// bf16 (RNE), fp32, or E4M3 codes of fl(y * r) (round to nearest even,
+// saturating: the element step of the static quantizer, on the fp32 value).
+// vec: the row pitch and base allow one aligned store.
+__device__ __attribute__((always_inline)) inline void store4(const GemmArgs& g, int m, int n, float v0, float v1,
+                                                             float v2, float v3, bool vec, float r) {
+  if (g.out_mode == OUT_F32) {
+    float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+    if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
+    else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
+  } else if (g.out_mode == OUT_FP8) {
+    const float y[4] = {__fmul_rn(v0, r), __fmul_rn(v1, r), __fmul_rn(v2, r), __fmul_rn(v3, r)};
+    const uint32_t w = hw_e4m3x4(y);
+    uint8_t* o = reinterpret_cast<uint8_t*>(g.y) + (int64_t)m * g.ldy + n;
+    if (vec) *reinterpret_cast<uint32_t*>(o) = w;
+    else { o[0] = (uint8_t)w; o[1] = (uint8_t)(w >> 8); o[2] = (uint8_t)(w >> 16); o[3] = (uint8_t)(w >> 24); }
+  } else {
+    uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+    const uint32_t w0 = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
+    const uint32_t w1 = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
+    if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
+    else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
+  }
+}
+
+// Whether store4 may use one aligned store for every row of this output.
+__device__ __attribute__((always_inline)) inline bool out_vec(const GemmArgs& g) {
+  const int esz = g.out_mode == OUT_F32 ? 4 : g.out_mode == OUT_FP8 ? 1 : 2;
+  return ((reinterpret_cast<uintptr_t>(g.y) & (4 * esz - 1)) == 0) && ((g.ldy & 3) == 0);
+}
 
 // LDS bytes per 32-row panel per 128-chunk: codes/values of A (activations)
 // and B (weights), and expanded block scales of A and B.
@@ -399,7 +440,8 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   // ---- epilogue: scale, round, store. Lane holds Y[m][n + 8 q .. +3] for q = 0..3.
   float c = *g.w_tscale;
   if (MODE != MODE_W4A16) c = c * *g.a_tscale;
-  const bool vec = ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 3) == 0);
+  const bool vec = out_vec(g);
+  const float ry = out_rscale(g);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int m = m0 + (wm * TM + i) * 32 + (lane & 31);
@@ -410,19 +452,8 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
       for (int qd = 0; qd < 4; ++qd) {
         const int n = n0 + (wn * TN + j) * 32 + 8 * qd + 4 * (lane >> 5);
         if (n >= g.n) continue;
-        const float v0 = acc[i][j][4 * qd] * c, v1 = acc[i][j][4 * qd + 1] * c;
-        const float v2 = acc[i][j][4 * qd + 2] * c, v3 = acc[i][j][4 * qd + 3] * c;
-        if (g.f32out) {
-          float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-          if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
-          else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
-        } else {
-          uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-          const uint32_t w0 = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
-          const uint32_t w1 = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
-          if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-          else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
-        }
+        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
+               acc[i][j][4 * qd + 3] * c, vec, ry);
       }
     }
   }
@@ -582,7 +613,8 @@ __global__ void __launch_bounds__(256) k_gemm_fp8(GemmArgs g) {
   }
 
   const float c = *g.w_tscale * *g.a_tscale;
-  const bool vec = ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 3) == 0);
+  const bool vec = out_vec(g);
+  const float ry = out_rscale(g);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int m = m0 + (wm * TM + i) * 32 + (lane & 31);
@@ -593,19 +625,8 @@ __global__ void __launch_bounds__(256) k_gemm_fp8(GemmArgs g) {
       for (int qd = 0; qd < 4; ++qd) {
         const int n = n0 + (wn * TN + j) * 32 + 8 * qd + 4 * gq;
         if (n >= g.n) continue;
-        const float v0 = acc[i][j][4 * qd] * c, v1 = acc[i][j][4 * qd + 1] * c;
-        const float v2 = acc[i][j][4 * qd + 2] * c, v3 = acc[i][j][4 * qd + 3] * c;
-        if (g.f32out) {
-          float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-          if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
-          else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
-        } else {
-          uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-          const uint32_t w0 = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
-          const uint32_t w1 = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
-          if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-          else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
-        }
+        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
+               acc[i][j][4 * qd + 3] * c, vec, ry);
       }
     }
   }
@@ -634,7 +655,8 @@ __device__ __attribute__((always_inline)) inline uint32_t pk_bf16(float a, float
 template <int TM, int TN>
 __device__ __attribute__((always_inline)) inline void store_tiles(const GemmArgs& g, const v16f (&acc)[TM][TN],
                                                                   int mw, int nw, int lane, float c) {
-  const bool vec = ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 3) == 0);
+  const bool vec = out_vec(g);
+  const float ry = out_rscale(g);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int m = mw + 32 * i + (lane & 31);
@@ -645,18 +667,8 @@ __device__ __attribute__((always_inline)) inline void store_tiles(const GemmArgs
       for (int qd = 0; qd < 4; ++qd) {
         const int n = nw + 32 * j + 8 * qd + 4 * (lane >> 5);
         if (n >= g.n) continue;
-        const float v0 = acc[i][j][4 * qd] * c, v1 = acc[i][j][4 * qd + 1] * c;
-        const float v2 = acc[i][j][4 * qd + 2] * c, v3 = acc[i][j][4 * qd + 3] * c;
-        if (g.f32out) {
-          float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-          if (vec) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
-          else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
-        } else {
-          uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-          const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
-          if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-          else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
-        }
+        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
+               acc[i][j][4 * qd + 3] * c, vec, ry);
       }
     }
   }
@@ -767,7 +779,7 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
   const int npanels_w = (g.n + 31) >> 5;
   const int total = g.tiles_m * g.tiles_n;
   const float scale = *g.w_tscale * *g.a_tscale;
-  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
   const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
   const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 4096), 0x00020000);
@@ -960,7 +972,7 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
   const int kcn = g.k >> 7;
   const int npanels_w = (g.n + 31) >> 5;
   const int total = g.tiles_m * g.tiles_n;
-  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
   const uint32_t ks = (uint32_t)(g.k >> 5);  // A scale bytes per row
   const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
   const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
@@ -1189,7 +1201,7 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   const int npanels_w = (g.n + 31) >> 5;
   const int total = g.tiles_m * g.tiles_n;
   const float scale = *g.w_tscale * *g.a_tscale;
-  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
   const uint32_t ka = (uint32_t)(g.k >> 1), ks = (uint32_t)(g.k >> 4);  // A code / scale bytes per row
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * ka), 0x00020000);
@@ -1446,7 +1458,7 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
   const int steps = g.k >> 6;
   const int npanels_w = (g.n + 31) >> 5;
   const int total = g.tiles_m * g.tiles_n;
-  const bool fast_out = !g.f32out && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
   const uint32_t ka = (uint32_t)(g.k >> 1), ks = (uint32_t)(g.k >> 5);  // A code / scale bytes per row
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * ka), 0x00020000);
@@ -1824,17 +1836,7 @@ __global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
       const int m = mb + 32 * i + (l & 31);
       const int n = (panel * NP + j) * 32 + 8 * q + 4 * (l >> 5);
       if (m >= g.m || n >= g.n) continue;
-      const float v0 = sum.x * c, v1 = sum.y * c, v2 = sum.z * c, v3 = sum.w * c;
-      if (g.f32out) {
-        float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-        if ((reinterpret_cast<uintptr_t>(o) & 15) == 0) *reinterpret_cast<float4*>(o) = make_float4(v0, v1, v2, v3);
-        else { o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3; }
-      } else {
-        uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-        const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
-        if ((reinterpret_cast<uintptr_t>(o) & 7) == 0) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-        else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
-      }
+      store4(g, m, n, sum.x * c, sum.y * c, sum.z * c, sum.w * c, out_vec(g), out_rscale(g));
     }
   }
 }
@@ -1925,15 +1927,8 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
         for (int qd = 0; qd < 4; ++qd) {
           const int n = panel * 32 + 8 * qd + 4 * gq;
           if (n >= g.n) continue;
-          const float v0 = acc[4 * qd] * c, v1 = acc[4 * qd + 1] * c, v2 = acc[4 * qd + 2] * c, v3 = acc[4 * qd + 3] * c;
-          if (g.f32out) {
-            float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-            o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3;
-          } else {
-            uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-            const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
-            o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16);
-          }
+          store4(g, m, n, acc[4 * qd] * c, acc[4 * qd + 1] * c, acc[4 * qd + 2] * c, acc[4 * qd + 3] * c, false,
+                 out_rscale(g));
         }
       }
     }
@@ -1942,11 +1937,12 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
   }
 }
 
-__global__ void k_zero_rows(void* y, int64_t m, int64_t n, int64_t ldy, int f32out) {
+__global__ void k_zero_rows(void* y, int64_t m, int64_t n, int64_t ldy, int out_mode) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= m * n) return;
   const int64_t r = t / n, c = t - r * n;
-  if (f32out) reinterpret_cast<float*>(y)[r * ldy + c] = 0.0f;
+  if (out_mode == OUT_F32) reinterpret_cast<float*>(y)[r * ldy + c] = 0.0f;
+  else if (out_mode == OUT_FP8) reinterpret_cast<uint8_t*>(y)[r * ldy + c] = 0;
   else reinterpret_cast<uint16_t*>(y)[r * ldy + c] = 0;
 }
 
@@ -1977,10 +1973,10 @@ static int device_cus() {
 
 hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const float* a_tscale,
                        int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
-                       void* y, int64_t ldy, bool f32out, hipStream_t st) {
+                       void* y, int64_t ldy, int out_mode, const float* y_scale, hipStream_t st) {
   if (m == 0 || n == 0) return hipSuccess;
   if (k == 0) {
-    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, m, n, ldy, (int)f32out);
+    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, m, n, ldy, out_mode);
     return hipGetLastError();
   }
   const int w_fmt = (a_fmt == 1 || a_fmt == 3 || a_fmt == 4) ? a_fmt : 2;
@@ -1997,7 +1993,8 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   g.k = (int)k;
   g.y = y;
   g.ldy = ldy;
-  g.f32out = f32out ? 1 : 0;
+  g.out_mode = out_mode;
+  g.y_scale = y_scale;
   g.tiles_m = g.tiles_n = 0;
   // persistent grids of 256 x 256 tiles, four waves of 128 x 128 each
   if (a_fmt == 4) {

@@ -203,9 +203,10 @@ qg_status qg_run_layers(const qg_stream_layer* layers, int32_t n_layers, void* c
       if (L.w_packed_bytes > slot_bytes) return QG_ERR_BUFFER_TOO_SMALL;
     }
     const bool bf16 = (L.a_fmt == QG_FMT_BF16);
+    if (L.y_dtype != QG_OUT_BF16 && L.y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
     const qg_status g = qg::check_gemm(L.a_fmt, bf16 ? L.x : L.a_codes, bf16 ? nullptr : L.a_block_scales,
                                        bf16 ? nullptr : L.a_tensor_scale, L.k, L.w_fmt, wdev, L.w_packed_bytes,
-                                       L.m, L.n, L.k, L.y, L.n, L.y_dtype);
+                                       L.m, L.n, L.k, L.y, L.n, L.y_dtype == QG_OUT_F32 ? 4 : 2);
     if (g != QG_OK) return g;
   }
   hipStream_t cs = reinterpret_cast<hipStream_t>(compute_stream);
@@ -237,7 +238,7 @@ qg_status qg_run_layers(const qg_stream_layer* layers, int32_t n_layers, void* c
     e = qg::launch_gemm((int)L.a_fmt, bf16 ? L.x : L.a_codes,
                         reinterpret_cast<const uint8_t*>(bf16 ? nullptr : L.a_block_scales),
                         bf16 ? nullptr : L.a_tensor_scale, L.k, reinterpret_cast<const uint8_t*>(wdev), L.m, L.n,
-                        L.k, L.y, L.n, L.y_dtype == QG_OUT_F32, cs);
+                        L.k, L.y, L.n, L.y_dtype == QG_OUT_F32 ? 1 : 0, nullptr, cs);
     if (e != hipSuccess) return qg::status_of(e);
     if (!L.resident && (e = hipEventRecord(free_ev, cs)) != hipSuccess) return qg::status_of(e);
   }

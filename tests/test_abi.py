@@ -225,3 +225,16 @@ def test_mx_dequant_validation():
     assert dq(MXFP4, out=P + 8) == INVALID                            # 16-byte stores
     assert dq(MXFP4, codes=P + 2) == INVALID                          # 4-byte code loads
     assert dq(MXFP8, codes=P + 4) == INVALID                          # 8-byte code loads
+
+
+def test_gemm_quant_validation():
+    def gq(a_fmt=FP8, w_fmt=FP8, abs_=None, ats=P, lda=256, y=P, ldy=64, ys=P, m=32, n=64, k=256, wbytes=1 << 24):
+        return q.qg_gemm_quant(a_fmt, P, abs_, ats, lda, w_fmt, P, wbytes, m, n, k, y, ldy, ys, stream=0, check=False)
+    assert gq(ys=None) == INVALID                      # the output's decode scale is required
+    assert gq(ys=P + 2) == INVALID
+    assert gq(a_fmt=FP8, w_fmt=NVFP4) == UNSUP
+    assert gq(n=40) == SHAPE
+    assert gq(ldy=32) == INVALID                       # ldy < n
+    assert gq(y=None) == INVALID
+    assert gq(wbytes=100) == SMALL
+    assert gq(ats=None) == INVALID                     # the GEMM's own operand checks

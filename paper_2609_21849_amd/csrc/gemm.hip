@@ -77,6 +77,14 @@ __device__ __attribute__((always_inline)) inline float out_rscale(const GemmArgs
   return (s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
 }
 
+// Two fp32 values to a pair of bf16 (low half = a), round to nearest even
+// (one v_cvt_pk_bf16_f32).
+__device__ __attribute__((always_inline)) inline uint32_t pk_bf16(float a, float b) {
+  typedef float v2f_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 v2bf_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f_t){a, b}, v2bf_t));
+}
+
 // Four consecutive outputs y[m][n .. n+3] (n % 4 == 0) in the output format:
 // bf16 (RNE), fp32, or E4M3 codes of fl(y * r) (round to nearest even,
 // saturating: the element step of the static quantizer, on the fp32 value).
@@ -95,8 +103,7 @@ __device__ __attribute__((always_inline)) inline void store4(const GemmArgs& g, 
     else { o[0] = (uint8_t)w; o[1] = (uint8_t)(w >> 8); o[2] = (uint8_t)(w >> 16); o[3] = (uint8_t)(w >> 24); }
   } else {
     uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-    const uint32_t w0 = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
-    const uint32_t w1 = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
+    const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
     if (vec) *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
     else { o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16); }
   }
@@ -641,14 +648,6 @@ static hipError_t run_fp8(GemmArgs g, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------- FP8, 256 x 256 tiles
-// Two fp32 values to a pair of bf16 (low half = a), round to nearest even
-// (one v_cvt_pk_bf16_f32).
-__device__ __attribute__((always_inline)) inline uint32_t pk_bf16(float a, float b) {
-  typedef float v2f_t __attribute__((ext_vector_type(2)));
-  typedef __bf16 v2bf_t __attribute__((ext_vector_type(2)));
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f_t){a, b}, v2bf_t));
-}
-
 // Epilogue shared by the FP8 kernels: a wave's TM x TN accumulator tiles,
 // first output row mw and column nw, scaled by c and rounded to the output
 // type. Lane l holds Y[mw + 32 i + l % 32][nw + 32 j + 8 q + 4 (l / 32) + e].
@@ -1927,8 +1926,15 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
         for (int qd = 0; qd < 4; ++qd) {
           const int n = panel * 32 + 8 * qd + 4 * gq;
           if (n >= g.n) continue;
-          store4(g, m, n, acc[4 * qd] * c, acc[4 * qd + 1] * c, acc[4 * qd + 2] * c, acc[4 * qd + 3] * c, false,
-                 out_rscale(g));
+          const float v0 = acc[4 * qd] * c, v1 = acc[4 * qd + 1] * c, v2 = acc[4 * qd + 2] * c, v3 = acc[4 * qd + 3] * c;
+          if (g.out_mode == OUT_F32) {
+            float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+            o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3;
+          } else {
+            uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+            const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
+            o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16);
+          }
         }
       }
     }
@@ -2028,7 +2034,8 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   } else {
     const int64_t npan_all = (n + 31) / 32;
     const int64_t xbytes = (m + 1) * (k * 2 + 16);
-    if (m <= 16 && npan_all >= 8 * (int64_t)device_cus() && xbytes <= 128 * 1024) {
+    // (bf16 and fp32 outputs only: FP8 outputs take the split-K kernel)
+    if (m <= 16 && npan_all >= 8 * (int64_t)device_cus() && xbytes <= 128 * 1024 && out_mode != OUT_FP8) {
       const unsigned grid = (unsigned)std::min<int64_t>(device_cus(), (npan_all + 7) / 8);
       hipLaunchKernelGGL((k_w4a16_stream<6>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
       return hipGetLastError();

@@ -107,8 +107,20 @@ __global__ void __launch_bounds__(256) k_amax_dense(const uint16_t* __restrict__
 // itself (count 1): every read happens before the barrier, the write after.
 __global__ void __launch_bounds__(256) k_finalize(const uint32_t* partial, int count, float* slot,
                                                   float divisor) {
+  // eight loads per thread in flight at once: the partials were just written
+  // by workgroups on every XCD, so each round trip is a far-cache latency
+  constexpr int U = 8;
   uint32_t m = 0;
-  for (int i = threadIdx.x; i < count; i += 256) m = max(m, partial[i]);
+  for (int base = 0; base < count; base += 256 * U) {
+    uint32_t v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = base + u * 256 + (int)threadIdx.x;
+      v[u] = (i < count) ? partial[i] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) m = max(m, v[u]);
+  }
   for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
   __shared__ uint32_t part[4];
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;

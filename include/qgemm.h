@@ -52,6 +52,10 @@
  *  - Non-finite inputs are outside the contract: a tensor holding inf/NaN
  *    gets a NaN tensor scale (a sentinel a caller can test) and
  *    unspecified codes.
+ *  - Debug logging: with the environment variable QG_LOG set (to anything
+ *    but "" or "0") when the library is first used, every qg_status entry
+ *    point writes one line to stderr with its name, its scalar arguments
+ *    and the status it returns. Off by default.
  */
 #ifndef QGEMM_H
 #define QGEMM_H

@@ -6,10 +6,13 @@
 // these checks can be exercised on a machine without a GPU.
 #include <hip/hip_runtime.h>
 
+#include <cstdarg>
+#include <cstdio>
 #include <limits>
 
 #include "checks.hpp"
 #include "kernels.hpp"
+#include "log.hpp"
 #include "qgemm.h"
 
 namespace {
@@ -115,6 +118,19 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
 
 qg_status status_of(hipError_t e) { return hip_status(e); }
 
+void log_call(const char* fn, qg_status st, const char* fmt, ...) {
+  char args[256];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(args, sizeof args, fmt, ap);
+  va_end(ap);
+  if (st == QG_ERR_HIP)
+    std::fprintf(stderr, "[qgemm] %s(%s) -> %s (hipError %d: %s)\n", fn, args, qg_status_string(st),
+                 g_last_hip_error, hipGetErrorString((hipError_t)g_last_hip_error));
+  else
+    std::fprintf(stderr, "[qgemm] %s(%s) -> %s\n", fn, args, qg_status_string(st));
+}
+
 }  // namespace qg
 
 extern "C" {
@@ -137,31 +153,43 @@ int qg_abi_version(void) { return QG_ABI_VERSION; }
 
 qg_status qg_quantize_act(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
                           void* codes, void* block_scales, float* tensor_scale, void* stream) {
-  const qg_status c = qg::check_quantize(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale);
-  if (c != QG_OK) return c;
-  return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
-                                        reinterpret_cast<uint8_t*>(codes),
-                                        reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
-                                        reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    const qg_status c = qg::check_quantize(fmt, x, rows, cols, ldx, codes, block_scales, tensor_scale);
+    if (c != QG_OK) return c;
+    return hip_status(qg::launch_quantize((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
+                                          reinterpret_cast<uint8_t*>(codes),
+                                          reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                          reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_quantize_act", st_, "fmt=%d rows=%lld cols=%lld ldx=%lld",
+                 (int)fmt, (long long)rows, (long long)cols, (long long)ldx);
+  return st_;
 }
 
 qg_status qg_quantize_act_static(qg_format fmt, const void* x, int64_t rows, int64_t cols, int64_t ldx,
                                  void* codes, void* block_scales, const float* tensor_scale, void* stream) {
-  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16 || is_mx(fmt)) return QG_ERR_UNSUPPORTED;
-  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
-  if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
-  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
-  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
-  if (rows > 0 && cols > 0) {
-    if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
-    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
-  }
-  return hip_status(qg::launch_quantize_static((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
-                                               reinterpret_cast<uint8_t*>(codes),
-                                               reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
-                                               reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_BF16 || is_mx(fmt)) return QG_ERR_UNSUPPORTED;
+    if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+    if (rows > 0 && ldx < cols) return QG_ERR_INVALID_ARG;
+    if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+    if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+    if (rows > 0 && cols > 0) {
+      if (x == nullptr || codes == nullptr || !aligned(x, 2)) return QG_ERR_INVALID_ARG;
+      if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+    }
+    return hip_status(qg::launch_quantize_static((int)fmt, reinterpret_cast<const uint16_t*>(x), rows, cols, ldx,
+                                                 reinterpret_cast<uint8_t*>(codes),
+                                                 reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                                 reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_quantize_act_static", st_, "fmt=%d rows=%lld cols=%lld ldx=%lld",
+                 (int)fmt, (long long)rows, (long long)cols, (long long)ldx);
+  return st_;
 }
 
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k) {
@@ -196,81 +224,113 @@ static qg_status check_pack_args(qg_format fmt, const void* codes, const void* b
 qg_status qg_pack_weights(qg_format fmt, const void* codes, const void* block_scales,
                           const float* tensor_scale, int64_t n, int64_t k, void* packed,
                           size_t packed_bytes, void* stream) {
-  const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
-  if (s != QG_OK) return s;
-  return hip_status(qg::launch_pack((int)fmt, reinterpret_cast<const uint8_t*>(codes),
-                                    reinterpret_cast<const uint8_t*>(block_scales), tensor_scale, n,
-                                    k, reinterpret_cast<uint8_t*>(packed),
-                                    reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
+    if (s != QG_OK) return s;
+    return hip_status(qg::launch_pack((int)fmt, reinterpret_cast<const uint8_t*>(codes),
+                                      reinterpret_cast<const uint8_t*>(block_scales), tensor_scale, n,
+                                      k, reinterpret_cast<uint8_t*>(packed),
+                                      reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_pack_weights", st_, "fmt=%d n=%lld k=%lld packed_bytes=%zu",
+                 (int)fmt, (long long)n, (long long)k, packed_bytes);
+  return st_;
 }
 
 qg_status qg_unpack_weights(qg_format fmt, const void* packed, size_t packed_bytes, int64_t n,
                             int64_t k, void* codes, void* block_scales, float* tensor_scale,
                             void* stream) {
-  const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
-  if (s != QG_OK) return s;
-  return hip_status(qg::launch_unpack((int)fmt, reinterpret_cast<const uint8_t*>(packed), n, k,
-                                      reinterpret_cast<uint8_t*>(codes),
-                                      reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
-                                      reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    const qg_status s = check_pack_args(fmt, codes, block_scales, tensor_scale, n, k, packed, packed_bytes);
+    if (s != QG_OK) return s;
+    return hip_status(qg::launch_unpack((int)fmt, reinterpret_cast<const uint8_t*>(packed), n, k,
+                                        reinterpret_cast<uint8_t*>(codes),
+                                        reinterpret_cast<uint8_t*>(block_scales), tensor_scale,
+                                        reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_unpack_weights", st_, "fmt=%d n=%lld k=%lld packed_bytes=%zu",
+                 (int)fmt, (long long)n, (long long)k, packed_bytes);
+  return st_;
 }
 
 qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
                   const float* a_tensor_scale, int64_t lda, qg_format w_fmt, const void* w_packed,
                   size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y, int64_t ldy,
                   qg_out_dtype y_dtype, void* stream) {
-  if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
-  const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
-                                     w_packed_bytes, m, n, k, y, ldy, y_dtype == QG_OUT_F32 ? 4 : 2);
-  if (c != QG_OK) return c;
-  return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
-                                    a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
-                                    n, k, y, ldy, y_dtype == QG_OUT_F32 ? 1 : 0, nullptr,
-                                    reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+    const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
+                                       w_packed_bytes, m, n, k, y, ldy, y_dtype == QG_OUT_F32 ? 4 : 2);
+    if (c != QG_OK) return c;
+    return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
+                                      a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
+                                      n, k, y, ldy, y_dtype == QG_OUT_F32 ? 1 : 0, nullptr,
+                                      reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_gemm", st_, "a_fmt=%d w_fmt=%d m=%lld n=%lld k=%lld lda=%lld ldy=%lld y_dtype=%d",
+                 (int)a_fmt, (int)w_fmt, (long long)m, (long long)n, (long long)k, (long long)lda,
+                 (long long)ldy, (int)y_dtype);
+  return st_;
 }
 
 qg_status qg_gemm_quant(qg_format a_fmt, const void* a, const void* a_block_scales, const float* a_tensor_scale,
                         int64_t lda, qg_format w_fmt, const void* w_packed, size_t w_packed_bytes, int64_t m,
                         int64_t n, int64_t k, void* y_codes, int64_t ldy, const float* y_scale, void* stream) {
-  if (y_scale == nullptr || !aligned(y_scale, 4)) return QG_ERR_INVALID_ARG;
-  const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
-                                     w_packed_bytes, m, n, k, y_codes, ldy, 1);
-  if (c != QG_OK) return c;
-  return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
-                                    a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
-                                    n, k, y_codes, ldy, 2, y_scale, reinterpret_cast<hipStream_t>(stream)));
+  const qg_status st_ = [&]() -> qg_status {
+    if (y_scale == nullptr || !aligned(y_scale, 4)) return QG_ERR_INVALID_ARG;
+    const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
+                                       w_packed_bytes, m, n, k, y_codes, ldy, 1);
+    if (c != QG_OK) return c;
+    return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
+                                      a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
+                                      n, k, y_codes, ldy, 2, y_scale, reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_gemm_quant", st_, "a_fmt=%d w_fmt=%d m=%lld n=%lld k=%lld lda=%lld ldy=%lld",
+                 (int)a_fmt, (int)w_fmt, (long long)m, (long long)n, (long long)k, (long long)lda,
+                 (long long)ldy);
+  return st_;
 }
 
 qg_status qg_dequant(qg_format fmt, const void* codes, const void* block_scales,
                      const float* tensor_scale, int64_t rows, int64_t cols, void* out,
                      qg_out_dtype out_dtype, void* stream) {
-  if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
-  if (out_dtype != QG_OUT_BF16 && out_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
-  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
-  if (is_mx(fmt)) {
-    if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
-    if (cols % 32 != 0) return QG_ERR_SHAPE;
-    if (rows > 0 && cols > 0 &&
-        (codes == nullptr || block_scales == nullptr || out == nullptr || !aligned(codes, mx_code_align(fmt)) ||
-         !aligned(out, 16)))
-      return QG_ERR_INVALID_ARG;
+  const qg_status st_ = [&]() -> qg_status {
+    if (!valid_fmt(fmt)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;
+    if (out_dtype != QG_OUT_BF16 && out_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return QG_ERR_INVALID_ARG;
+    if (is_mx(fmt)) {
+      if (tensor_scale != nullptr) return QG_ERR_INVALID_ARG;
+      if (cols % 32 != 0) return QG_ERR_SHAPE;
+      if (rows > 0 && cols > 0 &&
+          (codes == nullptr || block_scales == nullptr || out == nullptr || !aligned(codes, mx_code_align(fmt)) ||
+           !aligned(out, 16)))
+        return QG_ERR_INVALID_ARG;
+      return hip_status(qg::launch_dequant((int)fmt, reinterpret_cast<const uint8_t*>(codes),
+                                           reinterpret_cast<const uint8_t*>(block_scales), nullptr, rows, cols,
+                                           out, out_dtype == QG_OUT_F32, reinterpret_cast<hipStream_t>(stream)));
+    }
+    if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
+    if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+    if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
+    if (rows > 0 && cols > 0) {
+      if (codes == nullptr || out == nullptr || !aligned(out, out_dtype == QG_OUT_F32 ? 4 : 2))
+        return QG_ERR_INVALID_ARG;
+      if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
+    }
     return hip_status(qg::launch_dequant((int)fmt, reinterpret_cast<const uint8_t*>(codes),
-                                         reinterpret_cast<const uint8_t*>(block_scales), nullptr, rows, cols,
-                                         out, out_dtype == QG_OUT_F32, reinterpret_cast<hipStream_t>(stream)));
-  }
-  if (fmt == QG_FMT_NVFP4 && cols % 16 != 0) return QG_ERR_SHAPE;
-  if (tensor_scale == nullptr || !aligned(tensor_scale, 4)) return QG_ERR_INVALID_ARG;
-  if (fmt == QG_FMT_FP8_E4M3 && block_scales != nullptr) return QG_ERR_INVALID_ARG;
-  if (rows > 0 && cols > 0) {
-    if (codes == nullptr || out == nullptr || !aligned(out, out_dtype == QG_OUT_F32 ? 4 : 2))
-      return QG_ERR_INVALID_ARG;
-    if (fmt == QG_FMT_NVFP4 && (block_scales == nullptr || !aligned(codes, 8))) return QG_ERR_INVALID_ARG;
-  }
-  return hip_status(qg::launch_dequant((int)fmt, reinterpret_cast<const uint8_t*>(codes),
-                                       reinterpret_cast<const uint8_t*>(block_scales), tensor_scale,
-                                       rows, cols, out, out_dtype == QG_OUT_F32,
-                                       reinterpret_cast<hipStream_t>(stream)));
+                                         reinterpret_cast<const uint8_t*>(block_scales), tensor_scale,
+                                         rows, cols, out, out_dtype == QG_OUT_F32,
+                                         reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_dequant", st_, "fmt=%d rows=%lld cols=%lld out_dtype=%d",
+                 (int)fmt, (long long)rows, (long long)cols, (int)out_dtype);
+  return st_;
 }
 
 }  // extern "C"

@@ -90,12 +90,60 @@ def lib() -> ctypes.CDLL:
 
 
 def _p(t) -> int | None:
-    """Device pointer of a tensor (or an int pointer); None -> NULL."""
+    """Device pointer of a CUDA tensor (or an int pointer, passed as given);
+    None -> NULL. A tensor in host memory is refused: the kernels would
+    dereference its address on the GPU."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not getattr(t, "is_cuda", False):
+        raise ValueError("expected a CUDA tensor, got one on %s" % (getattr(t, "device", type(t).__name__),))
     return t.data_ptr()
+
+
+def _need(t, name: str, dtype, shape=None, device=None, dense: bool = True) -> None:
+    """Checks a tensor argument of the allocating helpers: on the GPU, of
+    `dtype`, of `shape` (if given), on `device` (if given), and dense
+    (contiguous) or at least unit-stride along its rows. The C ABI sees only
+    pointers and sizes, so a wrong element type or shape would otherwise
+    become an out-of-bounds access on the GPU."""
+    if t is None or not getattr(t, "is_cuda", False):
+        raise ValueError("%s: expected a CUDA tensor, got %r" % (name, getattr(t, "device", t)))
+    if t.dtype != dtype:
+        raise ValueError("%s: expected dtype %s, got %s" % (name, dtype, t.dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s: expected shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if device is not None and t.device != device:
+        raise ValueError("%s: on %s, expected %s" % (name, t.device, device))
+    if dense and not t.is_contiguous():
+        raise ValueError("%s: expected a contiguous tensor" % name)
+    if not dense and (t.dim() != 2 or t.stride(1) != 1):
+        raise ValueError("%s: expected a 2-D tensor with unit stride along its rows" % name)
+
+
+def _need_q(q) -> None:
+    """Checks a QTensor: codes, block scales and tensor scale of the shapes
+    and types its format defines, all on one GPU."""
+    import torch
+    if not isinstance(q, QTensor):
+        raise ValueError("expected a QTensor, got %s" % type(q).__name__)
+    r, c = q.rows, q.cols
+    code_cols = c if q.fmt in (QG_FMT_FP8_E4M3, QG_FMT_MXFP8) else c // 2
+    _need(q.codes, "codes", torch.uint8, (r, code_cols))
+    dev = q.codes.device
+    if q.fmt == QG_FMT_FP8_E4M3:
+        if q.block_scales is not None:
+            raise ValueError("FP8 tensors have no block scales")
+    else:
+        _need(q.block_scales, "block_scales", torch.uint8, (r, c // (32 if q.fmt in MX_FORMATS else 16)), dev)
+    if q.fmt in MX_FORMATS:
+        if q.tensor_scale is not None:
+            raise ValueError("MX tensors have no tensor scale")
+    else:
+        _need(q.tensor_scale, "tensor_scale", torch.float32, None, dev)
+        if q.tensor_scale.numel() < 1:
+            raise ValueError("tensor_scale: expected one element")
 
 
 def _stream(stream) -> int | None:
@@ -168,15 +216,8 @@ def linear_fp8_out(a, w_packed, w_fmt: int, n: int, y_scale, stream=None) -> "QT
     """Y = A . W^T written as FP8 E4M3 codes with the static decode scale
     y_scale (a one-element fp32 CUDA tensor): the next linear's activation."""
     import torch
-    if isinstance(a, QTensor):
-        m, k, a_fmt = a.rows, a.cols, a.fmt
-        a_data, a_bs, a_ts, lda = a.codes, a.block_scales, a.tensor_scale, a.cols
-        dev = a.codes.device
-    else:
-        m, k = a.shape
-        a_fmt, a_data, a_bs, a_ts = QG_FMT_BF16, a, None, None
-        lda = a.stride(0) if m > 1 else k
-        dev = a.device
+    m, k, a_fmt, a_data, a_bs, a_ts, lda, dev = _operands(a, w_packed)
+    _need(y_scale, "y_scale", torch.float32, None, dev)
     codes = torch.empty((m, n), dtype=torch.uint8, device=dev)
     qg_gemm_quant(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, codes, n, y_scale,
                   stream)
@@ -266,9 +307,13 @@ def quantize(x, fmt: int, stream=None, static_scale=None) -> QTensor:
     With static_scale (a one-element fp32 CUDA tensor holding a calibrated
     decode scale) the scale is used as given instead of derived from x."""
     import torch
-    assert x.dtype == torch.bfloat16 and x.dim() == 2 and x.stride(1) == 1
+    _need(x, "x", torch.bfloat16, dense=False)
     rows, cols = x.shape
     dev = x.device
+    if static_scale is not None:
+        _need(static_scale, "static_scale", torch.float32, None, dev)
+        if static_scale.numel() < 1:
+            raise ValueError("static_scale: expected one element")
     if fmt == QG_FMT_FP8_E4M3:
         codes = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
         bs = None
@@ -293,6 +338,7 @@ def quantize(x, fmt: int, stream=None, static_scale=None) -> QTensor:
 def pack(q: QTensor, stream=None):
     """Pack a quantized weight [n, k] for qg_gemm; returns a uint8 CUDA tensor."""
     import torch
+    _need_q(q)
     nbytes = qg_packed_bytes(q.fmt, q.rows, q.cols)
     if nbytes == 0:
         raise QGError(3, "qg_packed_bytes")
@@ -303,6 +349,7 @@ def pack(q: QTensor, stream=None):
 
 def unpack(packed, fmt: int, n: int, k: int, stream=None) -> QTensor:
     import torch
+    _need(packed, "packed", torch.uint8)
     dev = packed.device
     if fmt == QG_FMT_FP8_E4M3:
         codes, bs = torch.empty((n, k), dtype=torch.uint8, device=dev), None
@@ -317,20 +364,34 @@ def unpack(packed, fmt: int, n: int, k: int, stream=None) -> QTensor:
     return QTensor(fmt, codes, bs, ts, n, k)
 
 
+def _operands(a, w_packed):
+    """(m, k, a_fmt, data, block scales, tensor scale, lda, device) of a
+    linear's activation operand, checked, and the packed weight checked."""
+    import torch
+    if isinstance(a, QTensor):
+        _need_q(a)
+        dev = a.codes.device
+        out = (a.rows, a.cols, a.fmt, a.codes, a.block_scales, a.tensor_scale, a.cols, dev)
+    else:
+        _need(a, "a", torch.bfloat16, dense=False)
+        m, k = a.shape
+        dev = a.device
+        out = (m, k, QG_FMT_BF16, a, None, None, a.stride(0) if m > 1 else k, dev)
+    _need(w_packed, "w_packed", torch.uint8, None, dev)
+    return out
+
+
 def linear(a, w_packed, w_fmt: int, n: int, out_dtype: int = QG_OUT_BF16, y=None, stream=None):
     """Y = A . W^T for a quantized A (QTensor) or a bf16 A (torch tensor)."""
     import torch
-    if isinstance(a, QTensor):
-        m, k, a_fmt = a.rows, a.cols, a.fmt
-        a_data, a_bs, a_ts, lda = a.codes, a.block_scales, a.tensor_scale, a.cols
-        dev = a.codes.device
-    else:
-        m, k = a.shape
-        a_fmt, a_data, a_bs, a_ts = QG_FMT_BF16, a, None, None
-        lda = a.stride(0) if m > 1 else k
-        dev = a.device
+    m, k, a_fmt, a_data, a_bs, a_ts, lda, dev = _operands(a, w_packed)
+    if out_dtype not in (QG_OUT_BF16, QG_OUT_F32):
+        raise ValueError("out_dtype must be QG_OUT_BF16 or QG_OUT_F32")
+    ydt = torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16
     if y is None:
-        y = torch.empty((m, n), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16, device=dev)
+        y = torch.empty((m, n), dtype=ydt, device=dev)
+    else:
+        _need(y, "y", ydt, (m, n), dev, dense=False)
     ldy = y.stride(0) if m > 1 else n
     qg_gemm(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, y, ldy, out_dtype, stream)
     return y
@@ -338,6 +399,7 @@ def linear(a, w_packed, w_fmt: int, n: int, out_dtype: int = QG_OUT_BF16, y=None
 
 def dequantize(q: QTensor, out_dtype: int = QG_OUT_F32, stream=None):
     import torch
+    _need_q(q)
     out = torch.empty((q.rows, q.cols), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16,
                       device=q.codes.device)
     qg_dequant(q.fmt, q.codes, q.block_scales, q.tensor_scale, q.rows, q.cols, out, out_dtype, stream)

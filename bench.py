@@ -747,34 +747,52 @@ def weight_streaming_part(q, dit, M, blocks=8, steps=3):
         a_max = float(max(M * e["k"] * 2 + M * e["n"] * 2 for e in dit))   # bf16 input + output of a linear
         tmin = 2 * max(wb) + a_max
         full = sum(wb) + a_max
+        # the two ends first: every weight resident, every weight streamed
         plans = {}
-        for label, budget in (("resident_100", full), ("resident_75", a_max + 0.75 * sum(wb)),
-                              ("resident_50", a_max + 0.5 * sum(wb)), ("resident_25", a_max + 0.25 * sum(wb)),
-                              ("t_min", tmin)):
-            budget = max(budget, tmin)
-            st_, res, pred, dev = q.qg_stream_plan(wb, cs, 2, rate, budget, a_max)
-            meas = run(res, steps)
-            plans[label] = {"budget_mb": round(budget / 1e6, 1), "device_mb": round(dev / 1e6, 1),
-                            "resident_layers": int(sum(res)), "streamed_layers": nl - int(sum(res)),
-                            "predicted_ms": round(pred * 1e3, 3), "measured_ms": round(meas * 1e3, 3)}
-        # the two ends: every weight resident, every weight streamed
         plans["all_resident"] = {"device_mb": round(full / 1e6, 1), "resident_layers": nl, "streamed_layers": 0,
                                  "predicted_ms": round(sum(cs) * 1e3, 3),
                                  "measured_ms": round(run([1] * nl, steps) * 1e3, 3)}
         _, pred_all = q.qg_stream_simulate(wb, cs, [0] * nl, 2, rate, 3)
+        meas_all = run([0] * nl, steps)
+        # Calibration: the copy rate the model needs to reproduce the measured
+        # all-streamed step (copies share the GPU with the GEMMs there, so the
+        # rate is below the idle-GPU one); the model's step time falls
+        # monotonically with the rate, so bisection finds it.
+        lo_r, hi_r = rate / 20.0, rate * 2.0
+        for _ in range(60):
+            mid = 0.5 * (lo_r + hi_r)
+            if q.qg_stream_simulate(wb, cs, [0] * nl, 2, mid, 3)[1] > meas_all:
+                lo_r = mid
+            else:
+                hi_r = mid
+        rate_eff = 0.5 * (lo_r + hi_r)
         plans["all_streamed"] = {"device_mb": round(tmin / 1e6, 1), "resident_layers": 0, "streamed_layers": nl,
-                                 "predicted_ms": round(pred_all * 1e3, 3),
-                                 "measured_ms": round(run([0] * nl, steps) * 1e3, 3)}
+                                 "predicted_ms": round(pred_all * 1e3, 3), "measured_ms": round(meas_all * 1e3, 3)}
+        # plans under device budgets, chosen with the calibrated rate; the
+        # idle-GPU rate's prediction of the same plan is given beside it
+        for label, budget in (("resident_100", full), ("resident_75", a_max + 0.75 * sum(wb)),
+                              ("resident_50", a_max + 0.5 * sum(wb)), ("resident_25", a_max + 0.25 * sum(wb)),
+                              ("t_min", tmin)):
+            budget = max(budget, tmin)
+            st_, res, pred, dev = q.qg_stream_plan(wb, cs, 2, rate_eff, budget, a_max)
+            _, pred_idle = q.qg_stream_simulate(wb, cs, res, 2, rate, 3)
+            meas = run(res, steps)
+            plans[label] = {"budget_mb": round(budget / 1e6, 1), "device_mb": round(dev / 1e6, 1),
+                            "resident_layers": int(sum(res)), "streamed_layers": nl - int(sum(res)),
+                            "predicted_ms": round(pred * 1e3, 3), "predicted_idle_rate_ms": round(pred_idle * 1e3, 3),
+                            "measured_ms": round(meas * 1e3, 3)}
         lam = {dit[j]["name"]: round(cs[(j - 1) % len(dit)] * rate / wb[j], 3) for j in range(len(dit))}
-        out[kind] = {"layers": nl, "h2d_gbs": round(rate / 1e9, 1),
+        out[kind] = {"layers": nl, "h2d_gbs": round(rate / 1e9, 1), "h2d_gbs_calibrated": round(rate_eff / 1e9, 1),
                      "linear_us": {k_: round(v * 1e6, 1) for k_, v in lin_s.items()},
                      "weight_mb": {e["name"]: round(e["w_" + kind].numel() / 1e6, 2) for e in dit},
                      "lambda": lam, "t_min_mb": round(tmin / 1e6, 1), "all_resident_mb": round(full / 1e6, 1),
                      "delta_all_streamed_ms": round(sum(wb) / rate * 1e3, 3),
                      "plans": plans}
-    out["note"] = ("lambda = L M / W with L the compute of the preceding linear; delta_all_streamed = N W / M, the "
-                   "paper's overhead bound with no overlapped layer; predicted = qg_stream_simulate of the plan with "
-                   "the measured L and M")
+    out["note"] = ("lambda = L M / W with L the compute of the preceding linear and M the idle-GPU copy rate; "
+                   "delta_all_streamed = N W / M, the paper's overhead bound with no overlapped layer; "
+                   "h2d_gbs_calibrated = the rate at which qg_stream_simulate reproduces the measured all-streamed "
+                   "step; the budget plans are chosen and predicted with it (predicted_idle_rate_ms: the same plan "
+                   "at the idle-GPU rate); all_streamed.predicted_ms uses the idle-GPU rate")
     return out
 
 

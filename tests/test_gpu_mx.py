@@ -39,6 +39,10 @@ def random_finite_bf16(rows, cols, seed):
     b = np.where(finite, b, b & 0x807F).reshape(rows, cols)   # inf/NaN -> subnormal
     b[0, :32] = 0                                              # an all-zero block
     b[-1, -32:] = 0x8000                                       # a block of -0
+    # blocks whose largest magnitude lies below 2^-125 (bf16 exponent fields 0
+    # and 1): a random block almost never does, and they need the code clamped at 0
+    b[1, :32] &= 0x807F                                        # subnormals only
+    b[2, 32:64] = (b[2, 32:64] & 0x807F) | 0x0080              # exponent field 1
     return b
 
 

@@ -139,6 +139,27 @@ def test_power_of_two_scaling_and_sign_symmetry(fmt):
     del sign
 
 
+@pytest.mark.parametrize("fmt", ["mxfp4", "mxfp8"])
+def test_tiny_blocks_clamp_the_scale_code_at_zero(fmt):
+    # block maxima below 2^(emax - 127) (bf16 subnormals and the smallest
+    # normals) would need a negative code: it clamps to 0 and the elements
+    # are coded at the scale 2^-127 (exact rational reference)
+    rng = np.random.default_rng(11)
+    rows = []
+    for top in (2.0 ** -133, 2.0 ** -130, 1.5 * 2.0 ** -127, 1.5 * 2.0 ** -126, 1.75 * 2.0 ** -120):
+        v = rng.uniform(-1.0, 1.0, 32) * top
+        v[3] = -top                                     # the largest magnitude is negative
+        rows.append(v)
+    x = _bits(np.array(rows))
+    xf = synth.bf16_bits_to_f32(x)
+    codes, scales = oracle.quantize_mx(x, fmt)
+    el = _unpack(codes, fmt)
+    for i in range(len(rows)):
+        e, ref = _reference(xf[i], fmt)
+        assert scales[i, 0] == e and list(el[i]) == ref, (i, scales[i, 0], e)
+    assert scales[:4, 0].tolist() == [0, 0, 0, 0] if fmt == "mxfp4" else scales[:, 0].tolist() == [0] * 5
+
+
 def test_zero_block_and_signed_zero():
     x = _bits(np.array([[0.0] * 31 + [-0.0]]))
     c, s = oracle.quantize_mx(x, "mxfp4")

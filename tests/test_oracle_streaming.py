@@ -52,6 +52,17 @@ def test_lambda_below_one_is_copy_bound(n, lam):
     assert last - n * L <= S.delta_overhead(n, 0, w, rate) * (1 + 1e-12)
 
 
+@pytest.mark.parametrize("resident", [[0] * 6, [1, 0, 0, 1, 0, 0], [1, 1, 1, 0, 1, 1]])
+def test_delta_is_attained_when_compute_vanishes(resident):
+    # with (almost) no compute to hide behind, every streamed copy is exposed:
+    # the step is the copies alone, Delta = (N - K) W / M with K resident layers
+    n, w, rate, L = len(resident), 12e6, 50e9, 1e-12
+    last, _ = S.simulate([w] * n, [L] * n, resident, 2, rate, steps=4)
+    k = sum(resident)
+    # (the vanishing compute hides in the gaps between copies)
+    assert last == pytest.approx(S.delta_overhead(n, k, w, rate), rel=1e-9)
+
+
 def test_single_buffer_serialises_copy_and_compute():
     w, rate, n = 10e6, 40e9, 6
     tau, L = w / rate, 3e-4

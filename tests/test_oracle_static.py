@@ -89,3 +89,18 @@ def test_static_rejects_bad_scales_and_nonfinite():
     xn[0, 3] = 0x7F80
     with pytest.raises(oracle.NonFiniteInput):
         oracle.quantize_fp8_static(xn, 0.01)
+
+
+def test_static_scale_validity_boundaries():
+    # FP8: 0 or a normal fp32 (>= 2^-126), so that 1/s is finite. NVFP4: 0 or
+    # >= 2^-96, so that 1/(dec(s_b) s_t) is finite for the smallest block
+    # scale code (2^-9). Both sides of each boundary, and the next float down.
+    x = synth.normal_bf16(2, 16, 1.0, 0, 0)
+    oracle.quantize_fp8_static(x, np.float32(2.0 ** -126))
+    oracle.quantize_nvfp4_static(x, np.float32(2.0 ** -96))
+    for bad in (2.0 ** -127, np.nextafter(np.float32(2.0 ** -126), np.float32(0))):
+        with pytest.raises(ValueError):
+            oracle.quantize_fp8_static(x, np.float32(bad))
+    for bad in (2.0 ** -97, np.nextafter(np.float32(2.0 ** -96), np.float32(0))):
+        with pytest.raises(ValueError):
+            oracle.quantize_nvfp4_static(x, np.float32(bad))

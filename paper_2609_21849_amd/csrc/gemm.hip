@@ -790,14 +790,15 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
   v8i fa[2];
   v16f acc[4][4];
 
-  // Offsets of chunks past the last one get the top bit set: out of range
-  // for every valid or invalid base (a uniform OR, no branch in the loop).
-  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  // The chunk's byte offset is uniform, so it travels in the loads' scalar
+  // offset and costs no per-lane arithmetic. Prefetches past the last chunk
+  // re-read that chunk (in bounds; their data is never multiplied). Rows and
+  // panels outside the operands keep an out-of-range per-lane base.
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
   auto load_a = [&](int kc) __attribute__((always_inline)) {
-    const uint32_t hi = past(kc);
 #pragma unroll
     for (int it = 0; it < RA; ++it)
-      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + kc * 128) | hi, 0, 0);
+      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], kcl(kc) * 128, 0);
   };
   auto write_a = [&](uint8_t* st) __attribute__((always_inline)) {
 #pragma unroll
@@ -806,14 +807,13 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
   // weight fragments of chunk kc into set P: (step, panel) in load order
   auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
     constexpr int P = decltype(Pc)::value;
-    const uint32_t hi = past(kc);
+    const int so = kcl(kc) * 4096;
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const uint32_t o = (ob[j] + kc * 4096 + s * 2048) | hi;
-        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
-        const v4i hi = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
+        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + s * 2048, so, 0);
+        const v4i hi = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + s * 2048 + 1024, so, 0);
         fb[P][s][j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
       }
   };
@@ -849,7 +849,7 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
     // The LDS writes sit between the fragment reads in program order (the
     // compiler cannot tell the two stages apart, so it keeps LDS accesses in
     // that order); each activation load follows the write of its register.
-    const uint32_t a_hi = past(kc + 2);
+    const int a_so = kcl(kc + 2) * 128;
 #pragma unroll
     for (int f = 4; f < 7; ++f) {
       fa[(f + 1) & 1] = read_a_frag(cur, wm * 4 + ((f + 1) & 3), (f + 1) >> 2, lane);
@@ -859,7 +859,7 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
       mgroup(Pc, f);
 #pragma unroll
       for (int it = 3 * (f - 4); it < 3 * (f - 3) && it < RA; ++it)
-        ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + (kc + 2) * 128) | a_hi, 0, 0);
+        ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], a_so, 0);
     }
 #pragma unroll
     for (int f = 4; f < 7; ++f) {

@@ -1477,12 +1477,15 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
   v4i fa[4];           // activation fragments, ring over MFMA groups (read two groups ahead)
   v16f acc[4][4];
 
-  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  // Chunk and step offsets are uniform: they travel in the loads' scalar
+  // offset, clamped to the last chunk / step (prefetches past the end re-read
+  // it in bounds; their data is never multiplied). Rows and panels outside
+  // the operands keep an out-of-range per-lane base.
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
   auto load_a = [&](int kc) __attribute__((always_inline)) {
-    const uint32_t hi = past(kc);
 #pragma unroll
-    for (int it = 0; it < 8; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[it] + kc * 128) | hi, 0, 0);
-    const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + kc * 8) | hi, 0, 0);
+    for (int it = 0; it < 8; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[it], kcl(kc) * 128, 0);
+    const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, osa, kcl(kc) * 8, 0);
     gs = make_uint2((uint32_t)t.x, (uint32_t)t.y);
   };
   // row scales of the chunk, blocks 0..7 -> [half 0: 0 2 4 6][half 1: 1 3 5 7]
@@ -1494,15 +1497,14 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
   // weight codes of global step t (= 4 x chunk + step) into ring slot S
   auto load_b = [&](auto Sc, int t) __attribute__((always_inline)) {
     constexpr int S = decltype(Sc)::value;
-    const uint32_t hi = t < steps ? 0u : OOB;
+    const int so = (t < steps ? t : steps - 1) * 1024;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[S][j] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, (ob[j] + t * 1024) | hi, 0, 0);
+    for (int j = 0; j < 4; ++j) fb[S][j] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j], so, 0);
   };
   auto load_bs = [&](auto Pc, int kc) __attribute__((always_inline)) {
     constexpr int P = decltype(Pc)::value;
-    const uint32_t hi = past(kc);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bsc[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + kc * 256) | hi, 0, 0);
+    for (int j = 0; j < 4; ++j) bsc[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, osb[j], kcl(kc) * 256, 0);
   };
   auto read_fa = [&](const uint8_t* st, int s, int i) __attribute__((always_inline)) {
     return *reinterpret_cast<const v4i*>(st + (wm * 4 + i) * 4096 + s * 1024 + ((lane ^ (2 * s + 9 * gq)) * 16));
@@ -1566,22 +1568,22 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
     pattern(std::integral_constant<int, 4>(), std::integral_constant<int, 8>(), I());
     // step 2: slot 1 refill; stage the activations of chunk kc + 1 (written
     // between the fragment reads in program order), then load those of kc + 2
-    const uint32_t a_hi = past(kc + 2);
+    const int a_so = kcl(kc + 2) * 128;
     load_b(std::integral_constant<int, 1>(), t0 + 5);
     [&]<int... F>(std::integer_sequence<int, F...>) {
       ((fa[(F + 10) & 3] = read_fa(cur, (F + 10) >> 2, (F + 10) & 3),
         *reinterpret_cast<v4i*>(nxt + la[2 * F]) = ga[2 * F],
         *reinterpret_cast<v4i*>(nxt + la[2 * F + 1]) = ga[2 * F + 1],
         mgroup(Pc, std::integral_constant<int, F + 8>()),
-        ga[2 * F] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[2 * F] + (kc + 2) * 128) | a_hi, 0, 0),
-        ga[2 * F + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[2 * F + 1] + (kc + 2) * 128) | a_hi, 0, 0)), ...);
+        ga[2 * F] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[2 * F], a_so, 0),
+        ga[2 * F + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[2 * F + 1], a_so, 0)), ...);
     }(std::make_integer_sequence<int, 4>());
     pattern(std::integral_constant<int, 4>(), std::integral_constant<int, 12>(), std::integral_constant<int, 8>());
     // step 3, first half: slot 2 refill, the row scales of chunk kc + 1
     load_b(std::integral_constant<int, 2>(), t0 + 6);
     write_a_scales(nxt);
     {
-      const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + (kc + 2) * 8) | a_hi, 0, 0);
+      const v2i t = __builtin_amdgcn_raw_buffer_load_b64(rs_as, osa, kcl(kc + 2) * 8, 0);
       gs = make_uint2((uint32_t)t.x, (uint32_t)t.y);
     }
     [&]<int... F>(std::integer_sequence<int, F...>) {

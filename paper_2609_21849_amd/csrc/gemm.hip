@@ -1222,12 +1222,15 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   v8h fa[2][4], fb[2][4];  // expanded fragments, two steps
   v16f acc[4][4];
 
-  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  // Chunk offsets are uniform: they travel in the loads' scalar offset,
+  // clamped to the last chunk (prefetches past the end re-read it in bounds;
+  // their data is never multiplied). Rows and panels outside the operands
+  // keep an out-of-range per-lane base.
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
   auto load_a = [&](int kc) __attribute__((always_inline)) {
-    const uint32_t hi = past(kc);
 #pragma unroll
-    for (int it = 0; it < 4; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[it] + kc * 64) | hi, 0, 0);
-    gs = __builtin_amdgcn_raw_buffer_load_b64(rs_as, (osa + kc * 8) | hi, 0, 0);
+    for (int it = 0; it < 4; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[it], kcl(kc) * 64, 0);
+    gs = __builtin_amdgcn_raw_buffer_load_b64(rs_as, osa, kcl(kc) * 8, 0);
   };
   auto write_a_codes = [&](uint8_t* st, int from, int to) __attribute__((always_inline)) {
 #pragma unroll
@@ -1240,13 +1243,12 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   };
   auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
     constexpr int P = decltype(Pc)::value;
-    const uint32_t hi = past(kc);
+    const int kq = kcl(kc);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t o = (ob[j] + kc * 2048) | hi;
-      bc[P][j][0] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
-      bc[P][j][1] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
-      bs[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + kc * 256) | hi, 0, 0);
+      bc[P][j][0] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j], kq * 2048, 0);
+      bc[P][j][1] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + 1024, kq * 2048, 0);
+      bs[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, osb[j], kq * 256, 0);
     }
   };
   auto read_a_half = [&](const uint8_t* st, int h) __attribute__((always_inline)) {

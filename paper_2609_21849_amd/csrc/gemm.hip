@@ -992,13 +992,16 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
   v8i fa[2];
   v16f acc[4][4];
 
-  auto past = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? 0u : OOB; };
+  // Chunk offsets are uniform: they travel in the loads' scalar offset,
+  // clamped to the last chunk (prefetches past the end re-read it in bounds;
+  // their data is never multiplied). Rows and panels outside the operands
+  // keep an out-of-range per-lane base.
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
   auto load_a = [&](int kc) __attribute__((always_inline)) {
-    const uint32_t hi = past(kc);
 #pragma unroll
     for (int it = 0; it < RA; ++it)
-      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + kc * 128) | hi, 0, 0);
-    gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (osa + kc * 4) | hi, 0, 0);
+      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], kcl(kc) * 128, 0);
+    gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, osa, kcl(kc) * 4, 0);
   };
   // blocks 0..3 of the chunk -> [half 0: 0 2][half 1: 1 3]
   auto write_a_scales = [&](uint8_t* st) __attribute__((always_inline)) {
@@ -1016,22 +1019,20 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
   };
   auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
     constexpr int P = decltype(Pc)::value;
-    const uint32_t hi = past(kc);
+    const int so = kcl(kc) * 4096;
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const uint32_t o = (ob[j] + kc * 4096 + s * 2048) | hi;
-        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, 0, 0);
-        const v4i hi2 = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, 0, 0);
+        const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + s * 2048, so, 0);
+        const v4i hi2 = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + s * 2048 + 1024, so, 0);
         fb[P][s][j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi2.x, hi2.y, hi2.z, hi2.w};
       }
   };
   // the weight scale dwords of the chunk pair starting at chunk kc (even)
   auto load_bs = [&](int kc) __attribute__((always_inline)) {
-    const uint32_t hi = past(kc);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bsn[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, (osb[j] + (kc >> 1) * 256) | hi, 0, 0);
+    for (int j = 0; j < 4; ++j) bsn[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, osb[j], (kcl(kc) >> 1) * 256, 0);
   };
   // MFMA group f = (step f / 4, activation panel f % 4); chunk parity P
   auto mgroup = [&](auto Pc, auto Fc) __attribute__((always_inline)) {
@@ -1065,7 +1066,7 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
     }
     __builtin_amdgcn_sched_barrier(0);
     // step 1, groups 4..6: stage activations of chunk kc + 1, load kc + 2
-    const uint32_t a_hi = past(kc + 2);
+    const int a_so = kcl(kc + 2);
     [&]<int... F>(std::integer_sequence<int, F...>) {
       ((fa[(F + 5) & 1] = read_a_frag(cur, wm * 4 + ((F + 5) & 3), (F + 5) >> 2, lane),
         [&] {
@@ -1077,8 +1078,8 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
         [&] {
 #pragma unroll
           for (int it = 3 * F; it < 3 * F + 3 && it < RA; ++it)
-            ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (A.oa[it] + (kc + 2) * 128) | a_hi, 0, 0);
-          if (F == 2) gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (osa + (kc + 2) * 4) | a_hi, 0, 0);
+            ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], a_so * 128, 0);
+          if (F == 2) gs = __builtin_amdgcn_raw_buffer_load_b32(rs_as, osa, a_so * 4, 0);
         }()), ...);
     }(std::make_integer_sequence<int, 3>());
 #pragma unroll

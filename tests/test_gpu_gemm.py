@@ -194,7 +194,7 @@ def test_w4a16_encoder_full(name, m):
     log("w4a16 %s m=%d max err/B" % (name, m), check_linear(y, oracle.linear_reference("w4a16", x, w)))
 
 
-@pytest.mark.parametrize("m,k", [(1, 1024), (7, 1024), (16, 1024), (15, 3072)])
+@pytest.mark.parametrize("m,k", [(1, 1024), (1, 3072), (7, 1024), (16, 1024), (15, 3072)])
 def test_w4a16_weight_pool_sampled(m, k):
     # a few activation rows against a very wide weight (a pool of stacked
     # encoder weights streamed once): the persistent streaming kernel, with a
@@ -207,6 +207,22 @@ def test_w4a16_weight_pool_sampled(m, k):
     rows, cols = _sample(m, n, 2000, 3)
     ref = oracle.linear_reference("w4a16", x, w, rows=rows, cols=cols)
     log("  max err/B", check_linear(y, ref, rows, cols))
+
+
+@pytest.mark.parametrize("out", [q.QG_OUT_F32, q.QG_OUT_BF16])
+def test_w4a16_one_row_wide_weight(out):
+    # one activation row against a very wide weight (the matrix-vector
+    # kernel): a half-filled last panel, heavy-tailed channels, subnormal and
+    # near-underflow activations, a zero block; every output against the oracle
+    n, k = 70032, 1024
+    log("w4a16 one row n=%d k=%d out=%d" % (n, k, out))
+    x = synth.normal_bf16(1, k, 1.0, 6, 0, synth.HEAVY_TAIL_FRAC, synth.HEAVY_TAIL_GAIN)
+    x[0, 16:32] &= 0x807F                          # subnormals only
+    x[0, 32:48] = (x[0, 32:48] & 0x807F) | 0x0080  # exponent field 1
+    x[0, 48:64] = 0
+    w = synth.normal_bf16(n, k, 0.02, 6, 1)
+    y = run_linear("w4a16", x, w, out=out)
+    log("  max err/B", check_linear(y, oracle.linear_reference("w4a16", x, w)))
 
 
 @pytest.mark.parametrize("kind", ["fp8", "nvfp4"])

@@ -49,6 +49,8 @@ def parse():
                          "for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT_MD"),
                     help="turn the two counter runs of --traffic-probe into the traffic summary")
+    ap.add_argument("--w4a16-pool-only", action="store_true",
+                    help="only the cold-HBM W4A16 pool measurement (one JSON line); for rocprofv3 runs")
     return ap.parse_args()
 
 
@@ -197,6 +199,9 @@ def main():
 
     q.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    if args.w4a16_pool_only:
+        print(json.dumps({"w4a16_cold_pool": w4a16_pool(q, synth, args.pool_mib)}), flush=True)
+        return
     t_setup = time.time()
 
     # ------------------------------------------------------------ inputs and offline weights

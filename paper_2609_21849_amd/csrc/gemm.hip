@@ -1849,22 +1849,34 @@ __global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
   }
 }
 
-// W4A16 with very few activation rows against a wide weight (a weight pool
-// streamed once): HBM-bound, so the weight stream is all that matters. A
-// persistent workgroup stages the activation rows in LDS once (row pitch
-// padded by 16 bytes, so that the rows of a fragment read fall in different
-// banks); each of its waves then owns whole 32-row weight panels (no split
-// of the reduction, no cross-wave reduction), walking the panel's chunks in
-// groups of D with the next group's weight loads issued before the current
-// group's MFMAs, so every wave keeps D chunks (D x 2.3 KiB) in flight. The
-// weights are read once, with non-temporal loads.
-// Lanes of activation rows past m read an extra all-zero row. Requires
-// m <= 32 and (m + 1) rows within the LDS budget (checked by the launcher).
-template <int D>
+// W4A16 with very few activation rows (2 .. 16) against a wide weight (a
+// weight pool streamed once): HBM-bound, so the weight stream is all that
+// matters. A persistent workgroup stages the activation rows in LDS once (row
+// pitch padded by 16 bytes, so that the rows of a fragment read fall in
+// different banks); each of its waves then owns whole 32-row weight panels
+// (no split of the reduction), walking the panel's chunks in groups of D with
+// the next group's weight loads issued before the current group's MFMAs, so
+// every wave keeps D chunks (D x 2.3 KiB) in flight. The weights are read
+// once, with non-temporal loads.
+//
+// Each MFMA step covers exactly one 16-block, so the block scale is applied
+// to the step's product instead of to every weight: the packed order gives
+// lane (r, g) the codes of k = 64 g + 8 s' + [0, 8) in dword s', and one
+// cross-half swap per dword pair (lanes 32..63 of dword 2 j with lanes 0..31
+// of dword 2 j + 1) leaves every lane with k = 16 s + 8 g + [0, 8) for step s
+// in dword s (j) and s + 4 (j + 4). The codes then decode straight to bf16
+// (one instruction per pair, no multiply), the activations are the A operand
+// (rows m), the weights the B operand (columns n = panel row r), and the
+// step's 32 x 32 product, computed from a zero accumulator, is added to the
+// MV useful rows of the running sum with the lane's own block scale (column
+// n): MV = 4 for m <= 8, 8 for m <= 16. Lanes of activation rows past m read
+// an extra all-zero row. Requires m <= 16 and (m + 1) rows within the LDS
+// budget (checked by the launcher).
+template <int D, int MV>
 __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
   constexpr uint32_t OOB = 0x80000000u;
   extern __shared__ __attribute__((aligned(16))) uint8_t xl[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 31, gq = lane >> 5;
   const int kcn = g.k >> 7;
   const int npan = (g.n + 31) >> 5;
@@ -1884,33 +1896,47 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npan * kcn * 2048), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npan * kcn * 256), 0x00020000);
-  const uint8_t* xrd = xl + min(r, g.m) * pitch + 128 * gq;  // + kc * 256 + s * 16
+  const uint8_t* xrd = xl + min(r, g.m) * pitch + 16 * gq;  // + kc * 256 + s * 32: k = 16 s + 8 g + [0, 8)
   const float c = *g.w_tscale;
-  struct W { v4i c0, c1; uint32_t sc; };
+  struct W { v4i c0, c1; uint2 sc; };
   W buf[2][D];
   auto load = [&](W (&b)[D], int panel, int kc0) __attribute__((always_inline)) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int kc = kc0 + d;
       const uint32_t o = (kc < kcn && panel < npan) ? (uint32_t)((panel * kcn + kc) * 2048 + lane * 16) : OOB;
-      const uint32_t os = (kc < kcn && panel < npan) ? (uint32_t)((panel * kcn + kc) * 256 + r * 8 + 4 * gq) : OOB;
+      const uint32_t os = (kc < kcn && panel < npan) ? (uint32_t)((panel * kcn + kc) * 256 + r * 8) : OOB;
       b[d].c0 = __builtin_amdgcn_raw_buffer_load_b128(rs_w, o, 0, kNT);
       b[d].c1 = __builtin_amdgcn_raw_buffer_load_b128(rs_w, o + 1024, 0, kNT);
-      b[d].sc = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, os, 0, kNT);
+      b[d].sc = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs_ws, os, 0, kNT));
     }
   };
-  v16f acc;
+  float acc[MV];
   auto compute = [&](const W (&b)[D], int kc0) __attribute__((always_inline)) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       if (kc0 + d >= kcn) break;
-      const uint32_t cw[8] = {(uint32_t)b[d].c0.x, (uint32_t)b[d].c0.y, (uint32_t)b[d].c0.z, (uint32_t)b[d].c0.w,
+      const uint32_t dw[8] = {(uint32_t)b[d].c0.x, (uint32_t)b[d].c0.y, (uint32_t)b[d].c0.z, (uint32_t)b[d].c0.w,
                               (uint32_t)b[d].c1.x, (uint32_t)b[d].c1.y, (uint32_t)b[d].c1.z, (uint32_t)b[d].c1.w};
+      uint32_t st[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const auto p = __builtin_amdgcn_permlane32_swap(dw[2 * j], dw[2 * j + 1], false, false);
+        st[j] = p[0];
+        st[j + 4] = p[1];
+      }
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        const v8bf wb = __builtin_bit_cast(v8bf, dequant8_bf16(cw[s], dec_e4m3_scale(b[d].sc >> (8 * (s >> 1)))));
-        const v4i xv = *reinterpret_cast<const v4i*>(xrd + (kc0 + d) * 256 + s * 16);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb, __builtin_bit_cast(v8bf, xv), acc, 0, 0, 0);
+        const uint4 wq = make_uint4(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 0)),
+                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 1)),
+                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 2)),
+                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 3)));
+        const uint4 xv = *reinterpret_cast<const uint4*>(xrd + (kc0 + d) * 256 + s * 32);
+        const v16f t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, xv), __builtin_bit_cast(v8bf, wq),
+                                                               (v16f){}, 0, 0, 0);
+        const float sc = dec_e4m3_scale((s < 4 ? b[d].sc.x : b[d].sc.y) >> (8 * (s & 3)));
+#pragma unroll
+        for (int v = 0; v < MV; ++v) acc[v] = __builtin_fmaf(t[v], sc, acc[v]);
       }
     }
   };
@@ -1924,27 +1950,21 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
     if (nk >= kcn) { np_ = panel + nw; nk = 0; }
     if (kc0 == 0)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+      for (int v = 0; v < MV; ++v) acc[v] = 0.0f;
     if (cur == 0) { load(buf[1], np_, nk); compute(buf[0], kc0); }
     else { load(buf[0], np_, nk); compute(buf[1], kc0); }
     cur ^= 1;
     if (nk == 0) {
-      // panel done: lane (r, g) holds rows r of columns 8q + 4g + e
-      const int m = r;
-      if (m < g.m) {
+      // panel done: lane (r, g) holds column n = 32 panel + r of rows 8 (v / 4) + 4 g + v % 4
+      const int n = panel * 32 + r;
+      if (n < g.n) {
 #pragma unroll
-        for (int qd = 0; qd < 4; ++qd) {
-          const int n = panel * 32 + 8 * qd + 4 * gq;
-          if (n >= g.n) continue;
-          const float v0 = acc[4 * qd] * c, v1 = acc[4 * qd + 1] * c, v2 = acc[4 * qd + 2] * c, v3 = acc[4 * qd + 3] * c;
-          if (g.out_mode == OUT_F32) {
-            float* o = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-            o[0] = v0; o[1] = v1; o[2] = v2; o[3] = v3;
-          } else {
-            uint16_t* o = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-            const uint32_t w0 = pk_bf16(v0, v1), w1 = pk_bf16(v2, v3);
-            o[0] = (uint16_t)w0; o[1] = (uint16_t)(w0 >> 16); o[2] = (uint16_t)w1; o[3] = (uint16_t)(w1 >> 16);
-          }
+        for (int v = 0; v < MV; ++v) {
+          const int m = 8 * (v >> 2) + 4 * gq + (v & 3);
+          if (m >= g.m) continue;
+          const float y = acc[v] * c;
+          if (g.out_mode == OUT_F32) reinterpret_cast<float*>(g.y)[(int64_t)m * g.ldy + n] = y;
+          else reinterpret_cast<uint16_t*>(g.y)[(int64_t)m * g.ldy + n] = (uint16_t)pk_bf16(y, 0.0f);
         }
       }
     }
@@ -2157,7 +2177,8 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
       const int64_t wmax = 8 * (int64_t)device_cus();
       const int64_t ppw = (npan_all + wmax - 1) / wmax;
       const unsigned grid = (unsigned)(((npan_all + ppw - 1) / ppw + 7) / 8);
-      hipLaunchKernelGGL((k_w4a16_stream<6>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<6, 4>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      else hipLaunchKernelGGL((k_w4a16_stream<6, 8>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
       return hipGetLastError();
     }
     if (m <= 1024) {

@@ -194,7 +194,7 @@ def test_w4a16_encoder_full(name, m):
     log("w4a16 %s m=%d max err/B" % (name, m), check_linear(y, oracle.linear_reference("w4a16", x, w)))
 
 
-@pytest.mark.parametrize("m,k", [(1, 1024), (1, 3072), (7, 1024), (16, 1024), (15, 3072)])
+@pytest.mark.parametrize("m,k", [(1, 1024), (1, 3072), (2, 3072), (7, 1024), (8, 1024), (9, 1024), (16, 1024), (15, 3072)])
 def test_w4a16_weight_pool_sampled(m, k):
     # a few activation rows against a very wide weight (a pool of stacked
     # encoder weights streamed once): the persistent streaming kernel, with a

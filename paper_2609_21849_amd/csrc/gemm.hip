@@ -1856,7 +1856,8 @@ __global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
 // different banks); each of its waves then owns whole 32-row weight panels
 // (no split of the reduction), walking the panel's chunks in groups of D with
 // the next group's weight loads issued before the current group's MFMAs, so
-// every wave keeps D chunks (D x 2.3 KiB) in flight. The weights are read
+// every wave keeps D chunks (D x 2.3 KiB) in flight (D = 4: six chunks
+// spill registers at m > 8 and are slower at m <= 8). The weights are read
 // once, with non-temporal loads.
 //
 // Each MFMA step covers exactly one 16-block, so the block scale is applied
@@ -1869,7 +1870,8 @@ __global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
 // (rows m), the weights the B operand (columns n = panel row r), and the
 // step's 32 x 32 product, computed from a zero accumulator, is added to the
 // MV useful rows of the running sum with the lane's own block scale (column
-// n): MV = 4 for m <= 8, 8 for m <= 16. Lanes of activation rows past m read
+// n), one step late, so that the FMAs do not wait on the MFMA just issued:
+// MV = 4 for m <= 8, 8 for m <= 16. Lanes of activation rows past m read
 // an extra all-zero row. Requires m <= 16 and (m + 1) rows within the LDS
 // budget (checked by the launcher).
 template <int D, int MV>
@@ -1925,18 +1927,26 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
         st[j] = p[0];
         st[j + 4] = p[1];
       }
+      // the row's eight block scales (E4M3, never negative or NaN), exactly
+      const v2f s01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc.x, false), s23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc.x, true);
+      const v2f s45 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc.y, false), s67 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc.y, true);
+      const float sc[8] = {s01[0], s01[1], s23[0], s23[1], s45[0], s45[1], s67[0], s67[1]};
+      // step s's product is scaled and summed after step s + 1's MFMA is issued
+      v16f t[2];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const uint4 wq = make_uint4(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 0)),
-                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 1)),
-                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 2)),
-                                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 3)));
-        const uint4 xv = *reinterpret_cast<const uint4*>(xrd + (kc0 + d) * 256 + s * 32);
-        const v16f t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, xv), __builtin_bit_cast(v8bf, wq),
-                                                               (v16f){}, 0, 0, 0);
-        const float sc = dec_e4m3_scale((s < 4 ? b[d].sc.x : b[d].sc.y) >> (8 * (s & 3)));
+      for (int s = 0; s <= 8; ++s) {
+        if (s < 8) {
+          const uint4 wq = make_uint4(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 0)),
+                                      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 1)),
+                                      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 2)),
+                                      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(st[s], 1.0f, 3)));
+          const uint4 xv = *reinterpret_cast<const uint4*>(xrd + (kc0 + d) * 256 + s * 32);
+          t[s & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, xv), __builtin_bit_cast(v8bf, wq),
+                                                             (v16f){}, 0, 0, 0);
+        }
+        if (s > 0)
 #pragma unroll
-        for (int v = 0; v < MV; ++v) acc[v] = __builtin_fmaf(t[v], sc, acc[v]);
+          for (int v = 0; v < MV; ++v) acc[v] = __builtin_fmaf(t[(s - 1) & 1][v], sc[s - 1], acc[v]);
       }
     }
   };
@@ -2177,8 +2187,8 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
       const int64_t wmax = 8 * (int64_t)device_cus();
       const int64_t ppw = (npan_all + wmax - 1) / wmax;
       const unsigned grid = (unsigned)(((npan_all + ppw - 1) / ppw + 7) / 8);
-      if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<6, 4>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
-      else hipLaunchKernelGGL((k_w4a16_stream<6, 8>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<4, 4>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      else hipLaunchKernelGGL((k_w4a16_stream<4, 8>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
       return hipGetLastError();
     }
     if (m <= 1024) {

@@ -2156,17 +2156,21 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     return hipGetLastError();
   }
   if (a_fmt == 1) {
-    if (m <= 128) return run_fp8<1, 2>(g, st);
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;
     const int tiles = g.tiles_m * g.tiles_n;
+    // Too few 256 x 256 tiles to fill the chip: the 64 x 128 kernel's eight
+    // times as many workgroups win. Measured crossover (encoder and
+    // transformer widths, M = 128 .. 3072): below 3/8 of a tile per CU.
+    if (m <= 128 || 8 * tiles < 3 * device_cus()) return run_fp8<1, 2>(g, st);
     hipLaunchKernelGGL(k_gemm_fp8_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
     return hipGetLastError();
   } else if (a_fmt == 2) {
-    if (m <= 128) return run<MODE_NVFP4, 2, 2, 1, 2>(g, st);
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;
     const int tiles = g.tiles_m * g.tiles_n;
+    // the same choice for W4A4; measured crossover: one tile per 8 CUs
+    if (m <= 128 || 8 * tiles <= device_cus()) return run<MODE_NVFP4, 2, 2, 1, 2>(g, st);
     hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
     return hipGetLastError();
   } else {

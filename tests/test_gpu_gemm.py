@@ -184,6 +184,22 @@ def test_dit_linear_sampled(kind, name):
     log("  max err/B", check_linear(y, ref, rows, cols))
 
 
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4"])
+@pytest.mark.parametrize("m,n,k", [(256, 3072, 1024), (512, 1024, 3072), (2048, 1024, 3072), (1530, 3072, 3072),
+                                   (2300, 3072, 3072), (3072, 3072, 1024)])
+def test_mid_m_linear_sampled(kind, m, n, k):
+    # token counts between the small-M shapes and the transformer's (ragged
+    # ones among them), on both sides of the tile-count thresholds that pick
+    # the 64 x 128 kernels (FP8, W4A4) over the persistent 256 x 256 ones
+    log("%s mid-m %dx%dx%d" % (kind, m, n, k))
+    x = synth.normal_bf16(m, k, 1.0, 7, 0)
+    w = synth.normal_bf16(n, k, 0.02, 7, 1)
+    y = run_linear(kind, x, w, check_codes=False)
+    rows, cols = _sample(m, n, 2000, 8)
+    ref = oracle.linear_reference(kind, x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))
+
+
 @pytest.mark.parametrize("name", list(synth.ENCODER_LINEARS))
 @pytest.mark.parametrize("m", synth.ENCODER_TOKENS)
 def test_w4a16_encoder_full(name, m):

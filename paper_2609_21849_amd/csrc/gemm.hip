@@ -1984,14 +1984,14 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
 }
 
 // W4A16 with one activation row against a wide weight: a matrix-vector
-// product, so no matrix instruction. The panel walk and the load pipeline are
-// those of k_w4a16_stream. In the packed order lane (r, g) holds, per chunk,
-// the 64 codes of weight row r at k = 64 g + [0, 64): four whole 16-blocks
-// (blocks 4 g .. 4 g + 3) with their four scale bytes. The lane decodes two
+// product, so no matrix instruction. The panel walk and the double-buffered
+// load groups are those of k_w4a16_stream. In the packed order lane (r, g)
+// holds, per chunk, the 64 codes of weight row r at k = 64 g + [0, 64): four
+// whole 16-blocks (blocks 4 g .. 4 g + 3) with their four scale bytes. The lane decodes two
 // codes per instruction to bf16, takes the dot product with the activation
 // pairs (one dot2 per pair, fp32 sum, subnormals kept), and multiplies each
 // block's partial sum by its E4M3 scale once, instead of scaling every
-// element (about 1.1 vector instructions per weight against 2 plus the MFMAs).
+// element: about 1.1 vector instructions per weight.
 // The two lanes of a row are summed at the end of the panel. The weights are
 // read once, with non-temporal loads (measured with the caches evicted before
 // every call: ~10% faster than ordinary loads). With 3 chunks per group the
@@ -2034,6 +2034,9 @@ __global__ void __launch_bounds__(512, 4) k_w4a16_gemv(GemmArgs g) {
       if (kc0 + d >= kcn) break;
       const uint32_t cw[8] = {(uint32_t)b[d].c0.x, (uint32_t)b[d].c0.y, (uint32_t)b[d].c0.z, (uint32_t)b[d].c0.w,
                               (uint32_t)b[d].c1.x, (uint32_t)b[d].c1.y, (uint32_t)b[d].c1.z, (uint32_t)b[d].c1.w};
+      // the four block scales (E4M3, never negative or NaN), exactly
+      const v2f s01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc, false), s23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)b[d].sc, true);
+      const float sc[4] = {s01[0], s01[1], s23[0], s23[1]};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {  // block 4 g + j: codes cw[2 j], cw[2 j + 1]
         float p = 0.0f;
@@ -2052,7 +2055,7 @@ __global__ void __launch_bounds__(512, 4) k_w4a16_gemv(GemmArgs g) {
           p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw[s], 1.0f, 3),
                                               __builtin_bit_cast(v2bf, xv.w), p, false);
         }
-        acc = __builtin_fmaf(p, dec_e4m3_scale(b[d].sc >> (8 * j)), acc);
+        acc = __builtin_fmaf(p, sc[j], acc);
       }
     }
   };

@@ -72,26 +72,31 @@ __global__ void __launch_bounds__(256) k_amax_partial(const uint16_t* __restrict
     partial[blockIdx.y * gridDim.x + blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
 }
 
-// Dense, 16-byte aligned tensors of `units` 8-element units: workgroup w
-// covers units [2048 w, 2048 w + 2048) as eight wave-contiguous runs and each
-// thread issues all eight of its 16-byte loads before the first max, so the
-// whole tensor is in flight at once instead of a few loads per thread.
+// Dense, 16-byte aligned tensors of `units` 8-element units: a grid of at most
+// kAmaxGroups workgroups strides over blocks of 1024 units, each block read
+// as four wave-contiguous runs with all four 16-byte loads of a thread issued
+// before the first max. Measured against one-shot grids (every workgroup one
+// block of 1024, 2048 or 4096 units): 3.5 us faster on a 4608 x 3072
+// activation, 1.3 us on 4608 x 9216.
+constexpr int64_t kAmaxGroups = 1024;  // four workgroups per CU on 256 CUs
+
 __global__ void __launch_bounds__(256) k_amax_dense(const uint16_t* __restrict__ x, int64_t units,
                                                     uint32_t* __restrict__ partial) {
-  constexpr int U = 8;
+  constexpr int U = 4;
   const uint4* xv = reinterpret_cast<const uint4*>(x);
-  const int64_t base = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
-  uint4 v[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) v[u] = (base + u * 256 < units) ? xv[base + u * 256] : make_uint4(0u, 0u, 0u, 0u);
   uint32_t m = 0;
+  for (int64_t base = (int64_t)blockIdx.x * 256 * U + threadIdx.x; base < units; base += (int64_t)gridDim.x * 256 * U) {
+    uint4 v[U];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    for (int u = 0; u < U; ++u) v[u] = (base + u * 256 < units) ? xv[base + u * 256] : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t t = w[i] & 0x7FFF7FFFu;
-      m = max(m, max(t & 0xFFFFu, t >> 16));
+    for (int u = 0; u < U; ++u) {
+      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t t = w[i] & 0x7FFF7FFFu;
+        m = max(m, max(t & 0xFFFFu, t >> 16));
+      }
     }
   }
   for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
@@ -547,7 +552,7 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
     const int64_t cap = (code_bytes - (int64_t)(base - reinterpret_cast<uintptr_t>(codes))) / 4;
     int64_t gx, gy;
     uint32_t* partial = reinterpret_cast<uint32_t*>(base);
-    const int64_t dense_groups = (c_eff / 8 + 2047) / 2048;
+    const int64_t dense_groups = std::min<int64_t>((c_eff / 8 + 1023) / 1024, kAmaxGroups);
     if (contig && vec && dense_groups <= cap) {
       gx = dense_groups;
       gy = 1;

@@ -365,6 +365,7 @@ def main():
     parts["weight_streaming"] = weight_streaming_part(q, dit, M)
     parts["w8a8_encoder"] = w8a8_encoder_part(q, enc)
     parts["w4a16_cold_pool"] = w4a16_pool(q, synth, args.pool_mib)
+    parts["single_linear"] = single_linear_part(q, synth)
 
     # dominant kernel: the GEMM kind with the largest share of the step, its
     # launches timed live inside the timed steps
@@ -378,11 +379,30 @@ def main():
                 "kernel": "k_gemm_fp8_direct (W8A8, fp8 MFMA)" if dom == "fp8" else "k_gemm_nvfp4_direct (W4A4, fp16 MFMA)",
                 "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic,
+                "frac_of_fp4_peak": round(achieved / PEAK["fp4"], 4) if dom == "nvfp4" else None,
                 "traffic_note": ("HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated), "
                                  "algorithmic %d" % tinfo["algorithmic_bytes_per_launch"]) if traffic else tinfo,
                 "avg_launch_us": round(1e3 * dur_ms / len(launches), 2), "launches": len(launches),
                 "flops_per_launch_avg": fl / len(launches)}
 
+    # per-format figures: the GEMMs of each format against their own peaks
+    # (NVFP4 against the fp4 peak first, and the fp16 matrix rate it runs on)
+    pool = parts["w4a16_cold_pool"]
+    sl = parts["single_linear"]
+    headline = {
+        "fp8_w8a8_dit_gemm_tflops": parts["fp8"]["gemm_tflops"],
+        "fp8_w8a8_frac_of_fp8_peak": parts["fp8"]["gemm_frac_of_fp8_peak"],
+        "nvfp4_w4a4_dit_gemm_tflops": parts["nvfp4"]["gemm_tflops"],
+        "nvfp4_w4a4_frac_of_fp4_peak": parts["nvfp4"]["gemm_frac_of_nvfp4_peak"],
+        "nvfp4_w4a4_frac_of_f16_mfma_peak": parts["nvfp4"]["gemm_frac_of_f16_mfma_peak"],
+        "w4a16_pool_m1_gbs": pool["m1"]["gbs"], "w4a16_pool_m1_frac_of_hbm": pool["m1"]["frac_of_hbm_peak"],
+        "w4a16_pool_m16_gbs": pool["m16"]["gbs"], "w4a16_pool_m16_frac_of_hbm": pool["m16"]["frac_of_hbm_peak"],
+        "w4a16_pool_m256_frac_of_bf16_peak": pool["m256"]["frac_of_bf16_peak"],
+        "w4a16_pool_m512_frac_of_bf16_peak": pool["m512"]["frac_of_bf16_peak"],
+        "c1_fp8_128x256x256_linear_us": sl["c1_fp8_128x256x256"]["linear_us"],
+        "c2_nvfp4_512x3072x3072_gemm_us": sl["c2_nvfp4_512x3072x3072"]["gemm_us"],
+        "c2_nvfp4_frac_of_roofline_f16_mfma": sl["c2_nvfp4_512x3072x3072"]["frac_of_roofline_f16_mfma"],
+    }
     value = total_flops / (step_ms * 1e9)
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "TFLOP/s", "n_gpus": 1,
@@ -395,6 +415,7 @@ def main():
                                "1024<->3072 at M in {1,16,256,512}",
                    "tokens": M, "seed": 0},
         "roofline": roofline,
+        "headline": headline,
         "parts": parts,
         "setup_s": round(t_setup, 1),
         "timed_wall_s": round(wall, 3),
@@ -402,6 +423,60 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def single_linear_part(q, synth, reps=50):
+    """The two single-linear configurations: FP8 W8A8 128x256x256 and NVFP4
+    W4A4 512x3072x3072 (X ~ N(0,1), W ~ N(0,0.02), seed 0), each call the
+    dynamic activation quantize plus the GEMM through the C ABI (the weight
+    quantized and packed offline). HIP events around each launch; medians
+    over `reps` calls. The NVFP4 GEMM is placed against its roofline:
+    max(2MNK / peak, algorithmic bytes / HBM peak) for the fp16 matrix rate
+    it runs on, and for the fp4 peak the format nominally targets."""
+    import torch
+    lib = q.lib()
+    st = torch.cuda.current_stream().cuda_stream
+    out = {}
+    for name, fmt, (m, n, k) in (("c1_fp8_128x256x256", q.QG_FMT_FP8_E4M3, (128, 256, 256)),
+                                 ("c2_nvfp4_512x3072x3072", q.QG_FMT_NVFP4, (512, 3072, 3072))):
+        x = dev_bf16(synth.normal_bf16(m, k, synth.SIGMA_X, 0, synth.STREAM_X))
+        w = dev_bf16(synth.normal_bf16(n, k, synth.SIGMA_W, 0, synth.STREAM_W))
+        packed = q.pack(q.quantize(w, fmt))
+        nv = fmt == q.QG_FMT_NVFP4
+        codes = torch.empty((m, k // 2 if nv else k), dtype=torch.uint8, device="cuda")
+        bs = torch.empty((m, k // 16), dtype=torch.uint8, device="cuda") if nv else None
+        ts = torch.empty(1, dtype=torch.float32, device="cuda")
+        y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+        bsp = bs.data_ptr() if nv else None
+        qargs = (fmt, x.data_ptr(), m, k, k, codes.data_ptr(), bsp, ts.data_ptr(), st)
+        gargs = (fmt, codes.data_ptr(), bsp, ts.data_ptr(), k, fmt, packed.data_ptr(), packed.numel(),
+                 m, n, k, y.data_ptr(), n, q.QG_OUT_BF16, st)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps + 5)]
+        for i in range(reps + 5):
+            evs[i][0].record()
+            assert lib.qg_quantize_act(*qargs) == 0
+            evs[i][1].record()
+            assert lib.qg_gemm(*gargs) == 0
+            evs[i][2].record()
+        torch.cuda.synchronize()
+        qus = float(np.median([ev[0].elapsed_time(ev[1]) for ev in evs[5:]])) * 1e3
+        gus = float(np.median([ev[1].elapsed_time(ev[2]) for ev in evs[5:]])) * 1e3
+        flops = 2.0 * m * n * k
+        wbytes = n * k * (0.5625 if nv else 1.0)
+        abytes = m * k * (0.5625 if nv else 1.0)
+        gbytes = wbytes + abytes + m * n * 2
+        ent = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2), "linear_us": round(qus + gus, 2),
+               "gemm_tflops": round(flops / (gus * 1e6), 1), "gemm_algorithmic_mb": round(gbytes / 1e6, 2)}
+        if nv:
+            t_f16 = max(flops / (PEAK["f16"] * 1e12), gbytes / (PEAK["hbm_gbs"] * 1e9)) * 1e6
+            t_fp4 = max(flops / (PEAK["fp4"] * 1e12), gbytes / (PEAK["hbm_gbs"] * 1e9)) * 1e6
+            ent.update({"roofline_us_f16_mfma": round(t_f16, 2), "frac_of_roofline_f16_mfma": round(t_f16 / gus, 4),
+                        "roofline_us_fp4": round(t_fp4, 2), "frac_of_roofline_fp4": round(t_fp4 / gus, 4)})
+        else:
+            ent["note"] = "16.8 MFLOP on 0.16 MB: launch-latency bound, reported in microseconds"
+        out[name] = ent
+        del packed, codes, bs, ts, y
+    return out
 
 
 def w8a8_encoder_part(q, enc, reps=20):
@@ -848,7 +923,8 @@ def static_scale_part(q, lib, st, dit, M, flops, steps=10):
 def w4a16_pool(q, synth, pool_mib):
     """Cold-HBM W4A16: M in {1, 16} against a pool of distinct encoder weights
     stacked along N (one call streams the whole pool once; pool > 2x the
-    256 MB last-level cache)."""
+    256 MB last-level cache): HBM-bound. M in {256, 512} over the same pool
+    is past the ridge point and reported against the bf16 matrix peak."""
     import torch
     n1, k1 = synth.ENCODER_LINEARS["down"]            # 1024 x 3072 per weight
     per = n1 * k1 * 0.5625
@@ -867,7 +943,7 @@ def w4a16_pool(q, synth, pool_mib):
     # a plain read of other memory before every timed call: back-to-back calls
     # over one pool can find part of it still in the 256 MB last-level cache
     evict = torch.ones(256 * 2 ** 20, dtype=torch.float32, device="cuda")
-    for m in (1, 16):
+    for m in (1, 16, 256, 512):
         x = dev_bf16(synth.normal_bf16(m, k1, synth.SIGMA_X, 0, 300 + m))
         y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
         fn = lambda: q.qg_gemm(q.QG_FMT_BF16, x, None, None, k1, q.QG_FMT_NVFP4, packed, packed.numel(),
@@ -896,36 +972,75 @@ def w4a16_pool(q, synth, pool_mib):
                           "frac_of_hbm_peak": round(byt / (ms * 1e6) / PEAK["hbm_gbs"], 4),
                           "us_back_to_back": round(ms_b2b * 1e3, 1),
                           "gbs_back_to_back": round(byt / (ms_b2b * 1e6), 1)}
+        if m >= 256:
+            # past the ridge point (bf16 315 flop/B): bound by the bf16 matrix rate
+            tf = 2.0 * m * n * k1 / (ms * 1e9)
+            res["m%d" % m].update({"tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK["bf16"], 4)})
     del packed, evict
     torch.cuda.empty_cache()
     return res
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(target_s: float):
-    """The CPU oracle (as it stands) on a bounded sample of the same workload:
-    NVFP4 quantization of a slice of the QKV activations plus the fp64
-    product of that slice with the quantized QKV weight."""
+    """The CPU oracle (as it stands) on a bounded sample of the NVFP4 QKV
+    linear of the step, on the same inputs as the GPU (heavy-tailed X
+    [4608, 3072], W [9216, 3072], seed 0): the activation quantization of the
+    whole tensor (one tensor scale over all 4608 rows, the codes the GPU
+    computes), its dequantization and the fp64 product for the first R rows.
+    The weight is quantized offline (not timed), as on the GPU. Rate =
+    2 R N K / (R/4608 of the full-tensor quantize + dequant + product of R
+    rows), measured with all host threads and with one thread; R is sized
+    so that the all-thread run takes about `target_s` seconds."""
     import oracle
     import synth
+    M = synth.DIT_TOKENS
     n, k = synth.DIT_LINEARS["qkv"]
+    x = synth.normal_bf16(M, k, synth.SIGMA_X, 0, synth.STREAM_X, synth.HEAVY_TAIL_FRAC, synth.HEAVY_TAIL_GAIN)
     w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, synth.STREAM_W)
     qw, bw, sw = oracle.quantize_nvfp4(w)
     wdeq = oracle.dequant_nvfp4(qw, bw, sw)
-    rows_done, t_spent, flops = 0, 0.0, 0.0
-    chunk = 8
-    while t_spent < target_s and rows_done < 4608:
-        x = synth.normal_bf16(chunk, k, 1.0, 0, 1000 + rows_done)
+    all_threads = oracle.num_threads()
+
+    def run(rows):
         t0 = time.time()
         qa, ba, sa = oracle.quantize_nvfp4(x)
-        a = oracle.dequant_nvfp4(qa, ba, sa)
+        t_q = time.time() - t0
+        t0 = time.time()
+        a = oracle.dequant_nvfp4(qa[:rows], ba[:rows], sa)
         oracle.gemm_f64(a, wdeq)
-        t_spent += time.time() - t0
-        rows_done += chunk
-        flops += 2.0 * chunk * n * k
-    return {"value": round(flops / t_spent / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": round(t_spent, 2),
-            "sample": "NVFP4 W4A4 QKV linear (N=9216, K=3072): %d of 4608 token rows, activation "
-                      "quantize + dequant + fp64 product; weight quantized offline" % rows_done}
+        t_p = time.time() - t0
+        return t_q, t_p
+
+    out = {"unit": "TFLOP/s", "kind": "oracle", "cpu_model": cpu_model(), "cores": all_threads}
+    # size R from a small probe, then time it with all threads and with one
+    oracle.set_num_threads(all_threads)
+    t_q, t_p = run(16)
+    rows = int(min(M, max(16, 16 * target_s / max(t_p + t_q * 16 / M, 1e-6))))
+    for label, threads, r in (("all_threads", all_threads, rows), ("single_thread", 1, max(8, rows // all_threads))):
+        oracle.set_num_threads(threads)
+        t_q, t_p = run(r)
+        t = t_q * r / M + t_p
+        out[label] = {"threads": threads, "rows": r, "seconds": round(t_p + t_q, 2),
+                      "full_tensor_quantize_s": round(t_q, 3), "product_s": round(t_p, 2),
+                      "tflops": round(2.0 * r * n * k / t / 1e12, 6)}
+    oracle.set_num_threads(all_threads)
+    out["value"] = out["all_threads"]["tflops"]
+    out["sample"] = ("NVFP4 W4A4 QKV linear (N=9216, K=3072, heavy-tailed X, seed 0): quantize of the whole "
+                     "4608 x 3072 activation (one tensor scale) + dequant + fp64 product of its first %d rows "
+                     "(all threads) / %d rows (one thread); weight quantized offline"
+                     % (out["all_threads"]["rows"], out["single_thread"]["rows"]))
+    return out
 
 
 if __name__ == "__main__":

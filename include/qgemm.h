@@ -51,7 +51,10 @@
  *    calls whose buffers overlap must be ordered by the caller's streams.
  *  - Non-finite inputs are outside the contract: a tensor holding inf/NaN
  *    gets a NaN tensor scale (a sentinel a caller can test) and
- *    unspecified codes.
+ *    unspecified codes. The MX formats have no tensor scale: a block holding
+ *    inf/NaN gets the E8M0 NaN code 255 as its block scale (the other blocks
+ *    are unaffected), unspecified element codes, a NaN dequantization, and
+ *    unspecified GEMM outputs wherever it takes part.
  *  - Debug logging: with the environment variable QG_LOG set (to anything
  *    but "" or "0") when the library is first used, every qg_status entry
  *    point writes one line to stderr with its name, its scalar arguments

@@ -80,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.qo_gemm_f64.argtypes = [P, P, I64, I64, I64, P, P]
         L.qo_gemm_f64_sampled.argtypes = [P, P, I64, P, P, I64, P, P]
         L.qo_num_threads.restype = ctypes.c_int
+        L.qo_set_num_threads.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
 
@@ -245,6 +246,11 @@ def gemm_f64_sampled(a: np.ndarray, w: np.ndarray, rows: np.ndarray, cols: np.nd
 
 def num_threads() -> int:
     return lib().qo_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (results do not depend on it)."""
+    lib().qo_set_num_threads(int(n))
 
 
 # ---------------------------------------------------------------- end-to-end references

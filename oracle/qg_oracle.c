@@ -550,3 +550,15 @@ int qo_num_threads(void)
     return 1;
 #endif
 }
+
+/* Thread count of the parallel loops above (timing of the CPU baseline in
+ * single-thread and all-core modes; the results do not depend on it). */
+void qo_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}

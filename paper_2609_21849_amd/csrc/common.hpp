@@ -111,6 +111,37 @@ __host__ __device__ inline _Float16 e4m3_to_f16(uint32_t c) {
 }
 
 // ---------------------------------------------------------------------------
+// Block-scale decoders of the GEMM kernels (E4M3 block scales are never
+// negative: the quantizer codes a magnitude). The test probe checks each of
+// them on all 128 non-negative codes against the E4M3 definition.
+// Value of a non-negative E4M3 block-scale code (never NaN: the quantizer
+// saturates at 448), exactly: its 7 bits placed at the top of the fp32
+// mantissa/exponent field are the value times 2^-120 -- normal codes become
+// normal fp32 numbers, subnormal codes denormal ones -- and one multiply by
+// 2^120 restores it.
+__device__ inline float dec_e4m3_scale(uint32_t c) {
+  return u2f((c & 0x7Fu) << 20) * 1.329227995784915872903807060280344576e36f;  // 2^120
+}
+
+// Four E4M3 block scales (one dword, block b in byte b; never negative) to
+// fp16, exact: the E4M3 bit pattern shifted into the fp16 field is the value
+// divided by 2^8 (normal and subnormal alike), and the multiply by 2^8 lands
+// in the fp16 normal range. Result: .x = blocks 0 and 1, .y = blocks 2 and 3.
+__device__ __attribute__((always_inline)) inline uint2 e4m3x4_to_f16x4(uint32_t d) {
+  const v2h k256 = {(_Float16)256.0f, (_Float16)256.0f};
+  const uint32_t lo = ((d & 0x7Fu) << 7) | ((d & 0x7F00u) << 15);
+  const uint32_t hi = ((d & 0x7F0000u) >> 9) | ((d & 0x7F000000u) >> 1);
+  return make_uint2(__builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, lo) * k256),
+                    __builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, hi) * k256));
+}
+
+// fp16 block scale b (0..3) of a lane's four.
+__device__ __attribute__((always_inline)) inline _Float16 scale_f16(uint2 sc, int b) {
+  const uint32_t w = (b < 2) ? sc.x : sc.y;
+  return __builtin_bit_cast(_Float16, (uint16_t)((b & 1) ? (w >> 16) : (w & 0xFFFFu)));
+}
+
+// ---------------------------------------------------------------------------
 // Hardware conversions used by the quantizers (gfx950). Both are checked on
 // the GPU against the integer encoders above over all 2^32 fp32 inputs:
 //   E2M1: v_cvt_scalef32_pk_fp4_f32 with scale 1.0 equals enc_e2m1 on every

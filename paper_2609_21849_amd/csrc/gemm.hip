@@ -7,8 +7,9 @@
 // Three operand modes, all on 32x32 MFMAs:
 //   W8A8  (FP8 x FP8)    : codes go straight into v_mfma_f32_32x32x64_f8f6f4
 //                          (OCP E4M3 operands); tensor scales in the epilogue.
-//                          Kernels of their own: k_gemm_fp8_direct for large
-//                          token counts, k_gemm_fp8 for small ones.
+//                          Kernels: k_gemm_fp8_direct for large token
+//                          counts, k_gemm_fp8 for mid-size ones, the split-K
+//                          k_gemm_splitk for few tokens.
 //   W4A4  (NVFP4 x NVFP4): the E4M3 block scale changes every 16 reduction
 //                          elements and is not a power of two, so it cannot
 //                          ride in the hardware's per-32 power-of-two operand
@@ -17,6 +18,8 @@
 //                          [2^-10, 2688]), so both operands are expanded to
 //                          fp16 in registers (v_cvt_scalef32_pk_f16_fp4 then
 //                          v_pk_mul_f16) and fed to v_mfma_f32_32x32x16_f16.
+//                          Kernels: k_gemm_nvfp4_direct for large token
+//                          counts, the split-K k_gemm_splitk below that.
 //   W4A16 (bf16 x NVFP4) : the weight is expanded the same way to bf16
 //                          (exact) for v_mfma_f32_32x32x16_bf16.
 //
@@ -30,7 +33,7 @@
 //   NVFP4, W4A16: elements [64 g, 64 g + 64) of its row over the chunk's
 //          eight 16-wide steps.
 //
-// Tiling of the shared NVFP4 / W4A16 template: a workgroup of WM x WN
+// Tiling of the large-M W4A16 kernel (k_gemm): a workgroup of WM x WN
 // wavefronts owns a (32 TM WM) x (32 TN WN) output tile; each wave owns
 // TM x TN tiles of 32 x 32. Chunks of 128 are staged in LDS in the packed
 // weight's lane-major order, so every LDS read is one contiguous 1 KiB wave
@@ -119,15 +122,23 @@ __device__ __attribute__((always_inline)) inline bool out_vec(const GemmArgs& g)
   return ((reinterpret_cast<uintptr_t>(g.y) & (4 * esz - 1)) == 0) && ((g.ldy & 3) == 0);
 }
 
-// LDS bytes per 32-row panel per 128-chunk: codes/values of A (activations)
-// and B (weights), and expanded block scales of A and B.
+// LDS bytes per 32-row panel per 128-chunk of the large-M W4A16 kernel:
+// bf16 activations (A), weight codes (B) and decoded weight block scales.
 template <int MODE> struct Lds;
-template <> struct Lds<MODE_NVFP4> { static constexpr int A = 2048, B = 2048, AS = 512, BS = 512; };
 template <> struct Lds<MODE_W4A16> { static constexpr int A = 8192, B = 2048, AS = 0, BS = 1024; };
 
 // 8 E2M1 codes (one dword) times an fp16 block scale -> 8 fp16 (exact).
 __device__ inline v8h dequant8_f16(uint32_t w, _Float16 sc) {
   const v2h s2 = {sc, sc};
+  const v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0) * s2;
+  const v2h p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1) * s2;
+  const v2h p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2) * s2;
+  const v2h p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3) * s2;
+  return (v8h){p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
+}
+
+// The same with the scale already in both halves of a register.
+__device__ __attribute__((always_inline)) inline v8h dequant8_f16x2(uint32_t w, v2h s2) {
   const v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0) * s2;
   const v2h p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1) * s2;
   const v2h p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2) * s2;
@@ -151,28 +162,6 @@ __device__ inline v4i dequant8_bf16(uint32_t w, float sc) {
   return o;
 }
 
-// Value of a non-negative E4M3 block-scale code (never NaN: the quantizer
-// saturates at 448), exactly: its 7 bits placed at the top of the fp32
-// mantissa/exponent field are the value times 2^-120 -- normal codes become
-// normal fp32 numbers, subnormal codes denormal ones -- and one multiply by
-// 2^120 restores it.
-__device__ inline float dec_e4m3_scale(uint32_t c) {
-  return u2f((c & 0x7Fu) << 20) * 1.329227995784915872903807060280344576e36f;  // 2^120
-}
-
-// 8 E4M3 block scales (two dwords, block j in byte j) -> 8 fp16 (exact).
-__device__ inline uint4 e4m3x8_to_f16(uint2 w) {
-  uint32_t h[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t d = (j < 2) ? w.x : w.y;
-    const uint32_t c0 = (d >> (16 * (j & 1))) & 0xFFu, c1 = (d >> (16 * (j & 1) + 8)) & 0xFFu;
-    h[j] = (uint32_t)__builtin_bit_cast(uint16_t, e4m3_to_f16(c0)) |
-           ((uint32_t)__builtin_bit_cast(uint16_t, e4m3_to_f16(c1)) << 16);
-  }
-  return make_uint4(h[0], h[1], h[2], h[3]);
-}
-
 // Output tile order: consecutive workgroups are dealt round-robin to the 8
 // XCDs (each with its own L2), so the linear id is remapped to give every XCD
 // a contiguous band of tiles, walked in groups of GROUP_M tile rows so that
@@ -193,20 +182,19 @@ __device__ inline void tile_coords(int id, int tiles_m, int tiles_n, int& bm, in
 
 template <int MODE, int WM, int WN, int TM, int TN, int DEPTH>
 __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
-  static_assert(MODE == MODE_NVFP4 || MODE == MODE_W4A16, "W8A8 has kernels of its own");
+  static_assert(MODE == MODE_W4A16, "W8A8 and W4A4 have kernels of their own");
   constexpr int NT = 64 * WM * WN;
   constexpr int PA = TM * WM, PB = TN * WN;  // 32-row panels per tile
   constexpr int BM = 32 * PA, BN = 32 * PB;
   constexpr int A_BYTES = PA * Lds<MODE>::A, B_BYTES = PB * Lds<MODE>::B;
   constexpr int AS_BYTES = PA * Lds<MODE>::AS, BS_BYTES = PB * Lds<MODE>::BS;
   constexpr int STAGE = A_BYTES + B_BYTES + AS_BYTES + BS_BYTES;
-  // 16-byte pieces per stage of each operand; one 8-byte scale run per row
+  // 16-byte pieces per stage of each operand; one 8-byte scale run per weight row
   constexpr int NPA = A_BYTES / 16, NPB = B_BYTES / 16;
   static_assert(NPA % NT == 0 && NPB % NT == 0, "piece count must divide the thread count");
   constexpr int RA = NPA / NT, RB = NPB / NT;
-  constexpr int NSA = (MODE == MODE_NVFP4) ? BM : 0;
   constexpr int NSB = BN;
-  constexpr int RSA = (NSA + NT - 1) / NT, RSB = (NSB + NT - 1) / NT;
+  constexpr int RSB = (NSB + NT - 1) / NT;
   constexpr int PIECES_A = Lds<MODE>::A / 16, PIECES_B = Lds<MODE>::B / 16;  // per panel chunk
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
@@ -223,13 +211,11 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   // each piece a thread copies is one 32-bit offset, the chunk advance is the
   // scalar offset, and rows or panels past the end fall outside the buffer's
   // range, which the hardware turns into zeros -- no branches, no clamping.
-  const int64_t a_row_bytes = (MODE == MODE_NVFP4) ? (int64_t)(g.k >> 1) : 2 * g.lda;
+  const int64_t a_row_bytes = 2 * g.lda;
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * a_row_bytes), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * Lds<MODE>::B), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rs_sa = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(g.a_bscale), 0, (MODE == MODE_NVFP4) ? (int)((int64_t)g.m * (g.k >> 4)) : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_sb = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
 
@@ -240,7 +226,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   // slot ((r + 32 g) ^ c) of LDS block h. The lanes of one row then hit
   // distinct LDS banks, and the operand read of lane l (slot l ^ (h + HALF g))
   // stays a conflict-free 1 KiB access.
-  constexpr int CPR = (MODE == MODE_NVFP4) ? 4 : 16;
+  constexpr int CPR = 16;
   constexpr int HALF = CPR / 2;
   uint32_t oa[RA];
   uint32_t la[RA];
@@ -261,13 +247,6 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
     const uint32_t panel = (uint32_t)((n0 >> 5) + p);
     ob[it] = (panel < (uint32_t)npanels_w) ? panel * (uint32_t)(kcn * Lds<MODE>::B) + 16u * s : 0x80000000u;
   }
-  uint32_t osa[RSA > 0 ? RSA : 1];
-#pragma unroll
-  for (int it = 0; it < RSA; ++it) {
-    const int q = it * NT + tid;
-    const uint32_t row = (uint32_t)(m0 + q);
-    osa[it] = (q < NSA && row < (uint32_t)g.m) ? row * (uint32_t)(g.k >> 4) : 0x80000000u;
-  }
   uint32_t osb[RSB > 0 ? RSB : 1];
 #pragma unroll
   for (int it = 0; it < RSB; ++it) {
@@ -279,19 +258,16 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   struct Regs {
     v4i a[RA > 0 ? RA : 1];
     v4i b[RB > 0 ? RB : 1];
-    v2i sa[RSA > 0 ? RSA : 1];
     v2i sb[RSB > 0 ? RSB : 1];
   };
 
   // ---- global -> registers for chunk kc
   auto load_chunk = [&](Regs& R, int kc) {
-    const int sa_off = (MODE == MODE_NVFP4) ? kc * 64 : kc * 256;
+    const int sa_off = kc * 256;
 #pragma unroll
     for (int it = 0; it < RA; ++it) R.a[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[it], sa_off, 0);
 #pragma unroll
     for (int it = 0; it < RB; ++it) R.b[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[it], kc * Lds<MODE>::B, 0);
-#pragma unroll
-    for (int it = 0; it < RSA; ++it) R.sa[it] = __builtin_amdgcn_raw_buffer_load_b64(rs_sa, osa[it], kc * 8, 0);
 #pragma unroll
     for (int it = 0; it < RSB; ++it) R.sb[it] = __builtin_amdgcn_raw_buffer_load_b64(rs_sb, osb[it], kc * 256, 0);
   };
@@ -300,31 +276,21 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   auto store_chunk = [&](const Regs& R, uint8_t* st) {
     uint8_t* sa = st;
     uint8_t* sb = st + A_BYTES;
-    uint8_t* ssa = st + A_BYTES + B_BYTES;
-    uint8_t* ssb = ssa + AS_BYTES;
+    uint8_t* ssb = st + A_BYTES + B_BYTES + AS_BYTES;
 #pragma unroll
     for (int it = 0; it < RA; ++it) *reinterpret_cast<v4i*>(sa + la[it]) = R.a[it];
 #pragma unroll
     for (int it = 0; it < RB; ++it) reinterpret_cast<v4i*>(sb)[it * NT + tid] = R.b[it];
 #pragma unroll
-    for (int it = 0; it < RSA; ++it) {
-      const int q = it * NT + tid;
-      if (q < NSA) reinterpret_cast<uint4*>(ssa)[q] = e4m3x8_to_f16(make_uint2(R.sa[it].x, R.sa[it].y));  // row q: 16 B
-    }
-#pragma unroll
     for (int it = 0; it < RSB; ++it) {
       const int q = it * NT + tid;
       if (q < NSB) {
-        if (MODE == MODE_NVFP4) {
-          reinterpret_cast<uint4*>(ssb)[q] = e4m3x8_to_f16(make_uint2(R.sb[it].x, R.sb[it].y));
-        } else {
-          const uint32_t w[2] = {(uint32_t)R.sb[it].x, (uint32_t)R.sb[it].y};
-          float f[8];
+        const uint32_t w[2] = {(uint32_t)R.sb[it].x, (uint32_t)R.sb[it].y};
+        float f[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) f[j] = dec_e4m3((w[j >> 2] >> (8 * (j & 3))) & 0xFFu);
-          reinterpret_cast<float4*>(ssb)[2 * q] = make_float4(f[0], f[1], f[2], f[3]);
-          reinterpret_cast<float4*>(ssb)[2 * q + 1] = make_float4(f[4], f[5], f[6], f[7]);
-        }
+        for (int j = 0; j < 8; ++j) f[j] = dec_e4m3((w[j >> 2] >> (8 * (j & 3))) & 0xFFu);
+        reinterpret_cast<float4*>(ssb)[2 * q] = make_float4(f[0], f[1], f[2], f[3]);
+        reinterpret_cast<float4*>(ssb)[2 * q + 1] = make_float4(f[4], f[5], f[6], f[7]);
       }
     }
   };
@@ -341,45 +307,9 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
   auto compute_chunk = [&](const uint8_t* st) {
     const uint8_t* sa = st;
     const uint8_t* sb = st + A_BYTES;
-    const uint8_t* ssa = st + A_BYTES + B_BYTES;
-    const uint8_t* ssb = ssa + AS_BYTES;
+    const uint8_t* ssb = st + A_BYTES + B_BYTES + AS_BYTES;
     const int r = lane & 31, gq = lane >> 5;
-    if (MODE == MODE_NVFP4) {
-      uint2 sca[TM], scb[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) sca[i] = *reinterpret_cast<const uint2*>(ssa + (wm * TM + i) * 512 + r * 16 + 8 * gq);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) scb[j] = *reinterpret_cast<const uint2*>(ssb + (wn * TN + j) * 512 + r * 16 + 8 * gq);
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {  // 16-byte half of each lane's codes: 4 MFMA steps
-        uint4 ca[TM], cb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          ca[i] = *reinterpret_cast<const uint4*>(sa + (wm * TM + i) * 2048 + hh * 1024 + ((lane ^ (hh + 2 * gq)) * 16));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) cb[j] = *reinterpret_cast<const uint4*>(sb + (wn * TN + j) * 2048 + hh * 1024 + lane * 16);
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-          const int s = 4 * hh + s4;  // blocks: scale index s / 2 of the lane's four
-          v8h fa[TM];
-#pragma unroll
-          for (int i = 0; i < TM; ++i) {
-            const uint32_t w = (s4 == 0) ? ca[i].x : (s4 == 1) ? ca[i].y : (s4 == 2) ? ca[i].z : ca[i].w;
-            const uint32_t sw = hh ? sca[i].y : sca[i].x;
-            fa[i] = dequant8_f16(w, __builtin_bit_cast(_Float16, (uint16_t)((s4 & 2) ? (sw >> 16) : (sw & 0xFFFFu))));
-          }
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const uint32_t w = (s4 == 0) ? cb[j].x : (s4 == 1) ? cb[j].y : (s4 == 2) ? cb[j].z : cb[j].w;
-            const uint32_t sw = hh ? scb[j].y : scb[j].x;
-            const v8h fb = dequant8_f16(w, __builtin_bit_cast(_Float16, (uint16_t)((s4 & 2) ? (sw >> 16) : (sw & 0xFFFFu))));
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb, fa[i], acc[i][j], 0, 0, 0);
-          }
-        }
-      }
-    } else {  // W4A16
+    {
       uint4 cb[TN][2];
       float4 scb[TN];
 #pragma unroll
@@ -450,7 +380,6 @@ __global__ void __launch_bounds__(64 * WM * WN) k_gemm(GemmArgs g) {
 
   // ---- epilogue: scale, round, store. Lane holds Y[m][n + 8 q .. +3] for q = 0..3.
   float c = *g.w_tscale;
-  if (MODE != MODE_W4A16) c = c * *g.a_tscale;
   const bool vec = out_vec(g);
   const float ry = out_rscale(g);
 #pragma unroll
@@ -648,6 +577,283 @@ static hipError_t run_fp8(GemmArgs g, hipStream_t st) {
   g.tiles_m = (g.m + 64 * TM - 1) / (64 * TM);
   g.tiles_n = (g.n + 64 * TN - 1) / (64 * TN);
   hipLaunchKernelGGL((k_gemm_fp8<TM, TN>), dim3(g.tiles_m * g.tiles_n), dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- W8A8 / W4A4, few tokens: split K
+// A workgroup owns a (32 MT) x (32 NP) output tile; its NW wavefronts split
+// the reduction dimension (128-wide chunk kc goes to wave kc % NW), each
+// wave accumulates the whole tile over its chunks, and the NW partial tiles
+// are summed through LDS at the end. So a tile costs a few chunks of one
+// wave, not K / 128 chunks in a row, and a short activation still keeps
+// every CU busy. Both operands go straight from memory into registers in
+// matrix-core operand order (no LDS staging, no barrier in the K loop):
+//   weights     : the packed image, one 16-byte piece per lane and register
+//                 half (plus, for NVFP4, one dword of four E4M3 block scales);
+//   activations : lane (r, g) reads row r's bytes of the permuted reduction
+//                 order directly: FP8 bytes [64 s + 32 g, +32) of step s,
+//                 NVFP4 bytes [32 g, 32 g + 32) of the chunk's 64 (elements
+//                 [64 g, 64 g + 64)) and its four block scales as one dword.
+// Every wave keeps D chunks in flight in a ring of register sets: the loads
+// of its chunk t + D are issued as soon as chunk t has been multiplied.
+// NVFP4 expands both operands to fp16 in registers (exact, as in k_gemm);
+// FP8 feeds the codes to the fp8 MFMA as they are.
+// Partial tiles go to LDS as row-major fp32 (row pitch 32 NP + 4 words, so
+// the 32 rows a store instruction touches spread over the banks), then
+// every thread sums four consecutive outputs of a row over the waves in a
+// fixed order (deterministic) and stores them: row-contiguous output writes.
+// When NW tiles do not fit in the LDS, waves NW/2.. first add theirs into
+// waves 0..NW/2-1 through it.
+// Tiles are dealt so that each XCD owns a contiguous range of weight panel
+// groups (its L2 then holds 1/8 of the weight and the whole activation).
+template <int MODE, int MT, int NP, int NW, int D>
+__global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
+  static_assert(MODE == MODE_FP8 || MODE == MODE_NVFP4, "W8A8 or W4A4");
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int BM = 32 * MT, BN = 32 * NP;
+  constexpr int LDR = BN + 4;  // fp32 row pitch of a partial tile in LDS
+  // partial tiles held in LDS at once: all NW, or NW / 2 when NW of them
+  // would not fit (the upper half of the waves then hands its tiles to the
+  // lower half first)
+  constexpr int NRED = (NW * BM * LDR * 4 <= 160 * 1024) ? NW : NW / 2;
+  static_assert(NRED * BM * LDR * 4 <= 160 * 1024, "partial tiles exceed the LDS");
+  __shared__ __attribute__((aligned(16))) float red[NRED * BM * LDR];
+  // the wave index is uniform across the wave: kept in a scalar register so
+  // that the chunk loop's bounds and branches are scalar too (a per-lane
+  // value there turns them into exec-masked regions, across which the
+  // compiler waits for every outstanding load)
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 31, gq = lane >> 5;
+  const int tiles = g.tiles_m * g.tiles_n;
+  const int t = (tiles % 8 == 0) ? (int)(blockIdx.x & 7) * (tiles >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
+  const int bn = t / g.tiles_m, bm = t - bn * g.tiles_m;
+  const int m0 = bm * BM, n0 = bn * BN;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+
+  const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * (MODE == MODE_FP8 ? 4096 : 2048)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, MODE == MODE_NVFP4 ? (int)((int64_t)npanels_w * kcn * 256) : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_a = (MODE == MODE_FP8)
+      ? rsrc_a_fp8(g)
+      : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * (g.k >> 1)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a_bscale), 0, MODE == MODE_NVFP4 ? (int)((int64_t)g.m * (g.k >> 4)) : 0, 0x00020000);
+
+  // per-lane base offsets (rows and panels outside the operands: out of range, zeros)
+  uint32_t oa[MT], oas[MT], ow[NP], ows[NP];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int row = m0 + 32 * i + r;
+    const bool in = row < g.m;
+    if (MODE == MODE_FP8) {
+      oa[i] = in ? (uint32_t)((int64_t)row * g.lda + 32 * gq) : OOB;
+      oas[i] = OOB;
+    } else {
+      oa[i] = in ? (uint32_t)(row * (g.k >> 1) + 32 * gq) : OOB;
+      oas[i] = in ? (uint32_t)(row * (g.k >> 4) + 4 * gq) : OOB;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NP; ++j) {
+    const int pj = (n0 >> 5) + j;
+    const bool in = pj < npanels_w;
+    ow[j] = in ? (uint32_t)(pj * kcn * (MODE == MODE_FP8 ? 4096 : 2048) + lane * 16) : OOB;
+    ows[j] = in ? (uint32_t)(pj * kcn * 256 + r * 8 + 4 * gq) : OOB;
+  }
+
+  // one 128-wide chunk of a lane's operands; FP8: piece 2 s + h = step s,
+  // register half h; NVFP4: pieces 0, 1 = the 32 code bytes, sc = 4 scales
+  struct Chunk {
+    v4i a[MT][MODE == MODE_FP8 ? 4 : 2];
+    v4i w[NP][MODE == MODE_FP8 ? 4 : 2];
+    uint32_t as[MODE == MODE_NVFP4 ? MT : 1];
+    uint32_t ws[MODE == MODE_NVFP4 ? NP : 1];
+  };
+  auto load = [&](Chunk& C, int kc) __attribute__((always_inline)) {
+    const uint32_t hi = kc < kcn ? 0u : OOB;
+    if (MODE == MODE_FP8) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {  // step p / 2, register half p % 2
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[i] + kc * 128 + (p >> 1) * 64 + (p & 1) * 16) | hi, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 4096 + p * 1024) | hi, 0, 0);
+      }
+    } else {
+      // in the order of use: block scales, then code halves 0 (steps 0..3)
+      // and 1 (steps 4..7), so each step waits only for what it reads
+#pragma unroll
+      for (int i = 0; i < MT; ++i) C.as[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (oas[i] + kc * 8) | hi, 0, 0);
+#pragma unroll
+      for (int j = 0; j < NP; ++j) C.ws[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, (ows[j] + kc * 256) | hi, 0, 0);
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[i] + kc * 64 + 16 * p) | hi, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 2048 + 1024 * p) | hi, 0, 0);
+      }
+    }
+    // keep each chunk's loads together and in this order: the waits before
+    // a chunk's MFMAs then leave the later chunks' loads in flight
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  v16f acc[MT][NP];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NP; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+  auto compute = [&](const Chunk& C) __attribute__((always_inline)) {
+    if (MODE == MODE_FP8) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        v8i fa[MT], fb[NP];
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          const v4i lo = C.a[i][2 * s], hi = C.a[i][2 * s + 1];
+          fa[i] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        }
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+          const v4i lo = C.w[j][2 * s], hi = C.w[j][2 * s + 1];
+          fb[j] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        }
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NP; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], 0, 0, 0, 0, 0, 0);
+      }
+    } else {
+      // the lane's four block scales as fp16, each in both halves of a register
+      v2h sa[MT][4], sw[NP][4];
+      auto dup = [&](uint32_t d, v2h (&o)[4]) __attribute__((always_inline)) {
+        const uint2 h = e4m3x4_to_f16x4(d);
+        o[0] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.x, h.x, 0x05040504u));
+        o[1] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.x, h.x, 0x07060706u));
+        o[2] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.y, h.y, 0x05040504u));
+        o[3] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.y, h.y, 0x07060706u));
+      };
+#pragma unroll
+      for (int i = 0; i < MT; ++i) dup(C.as[i], sa[i]);
+#pragma unroll
+      for (int j = 0; j < NP; ++j) dup(C.ws[j], sw[j]);
+      // step s: elements [64 g + 8 s, +8) of the chunk, block 4 g + s / 2;
+      // the expansion of step s + 1 is issued between the MFMAs of step s
+      v8h fa[2][MT], fb[2][NP];
+      auto expand = [&](int s, int set) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          const v4i c = C.a[i][s >> 2];
+          const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
+          fa[set][i] = dequant8_f16x2(w, sa[i][s >> 1]);
+        }
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+          const v4i c = C.w[j][s >> 2];
+          const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
+          fb[set][j] = dequant8_f16x2(w, sw[j][s >> 1]);
+        }
+      };
+      expand(0, 0);
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        if (s < 7) expand(s + 1, (s + 1) & 1);
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NP; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[s & 1][j], fa[s & 1][i], acc[i][j], 0, 0, 0);
+        if (s < 7) {
+          // each MFMA followed by its share of the next step's 8 (MT + NP)
+          // conversions and multiplies
+#pragma unroll
+          for (int t = 0; t < MT * NP; ++t) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, (8 * (MT + NP) + MT * NP - 1) / (MT * NP), 0);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  // this wave's chunks: kc = wave + NW t, t = 0 .. nt - 1
+  const int nt = (kcn - wave + NW - 1) / NW;
+  Chunk C[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(C[d], wave + NW * d);
+  for (int t0 = 0; t0 < nt; t0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      if (t0 + d < nt) compute(C[d]);
+      load(C[d], wave + NW * (t0 + d + D));
+    }
+  }
+
+  // partial tiles -> LDS (row-major fp32), then the sum over the waves
+  auto put = [&](float* part) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NP; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<float4*>(part + (32 * i + r) * LDR + 32 * j + 8 * q + 4 * gq) =
+              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+  };
+  if (NRED < NW) {
+    // waves NRED.. pass their tiles to waves 0..NRED-1 (wave w + NRED -> w)
+    if (wave >= NRED) put(red + (wave - NRED) * (BM * LDR));
+    __syncthreads();
+    if (wave < NRED) {
+      const float* part = red + wave * (BM * LDR);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 v = *reinterpret_cast<const float4*>(part + (32 * i + r) * LDR + 32 * j + 8 * q + 4 * gq);
+            acc[i][j][4 * q] += v.x; acc[i][j][4 * q + 1] += v.y; acc[i][j][4 * q + 2] += v.z; acc[i][j][4 * q + 3] += v.w;
+          }
+    }
+    __syncthreads();
+  }
+  if (wave < NRED) put(red + wave * (BM * LDR));
+  __syncthreads();
+  const float c = *g.w_tscale * *g.a_tscale;
+  const bool vec = out_vec(g);
+  const float ry = out_rscale(g);
+  for (int u = threadIdx.x; u < BM * (BN / 4); u += 64 * NW) {
+    const int row = u / (BN / 4), c4 = u - row * (BN / 4);
+    const int m = m0 + row, n = n0 + 4 * c4;
+    if (m >= g.m || n >= g.n) continue;
+    float4 sum = *reinterpret_cast<const float4*>(red + row * LDR + 4 * c4);
+#pragma unroll
+    for (int w = 1; w < NRED; ++w) {
+      const float4 v = *reinterpret_cast<const float4*>(red + w * (BM * LDR) + row * LDR + 4 * c4);
+      sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+    }
+    store4(g, m, n, sum.x * c, sum.y * c, sum.z * c, sum.w * c, vec, ry);
+  }
+}
+
+template <int MODE, int MT, int NP, int NW, int D>
+static hipError_t run_splitk(GemmArgs g, hipStream_t st) {
+  g.tiles_m = (g.m + 32 * MT - 1) / (32 * MT);
+  g.tiles_n = (g.n + 32 * NP - 1) / (32 * NP);
+  hipLaunchKernelGGL((k_gemm_splitk<MODE, MT, NP, NW, D>), dim3(g.tiles_m * g.tiles_n), dim3(64 * NW), 0, st, g);
   return hipGetLastError();
 }
 
@@ -1157,23 +1363,6 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------- W4A4 (NVFP4), large token counts
-// Four E4M3 block scales (one dword, block b in byte b; never negative) to
-// fp16, exact: the E4M3 bit pattern shifted into the fp16 field is the value
-// divided by 2^8 (normal and subnormal alike), and the multiply by 2^8 lands
-// in the fp16 normal range. Result: .x = blocks 0 and 1, .y = blocks 2 and 3.
-__device__ __attribute__((always_inline)) inline uint2 e4m3x4_to_f16x4(uint32_t d) {
-  const v2h k256 = {(_Float16)256.0f, (_Float16)256.0f};
-  const uint32_t lo = ((d & 0x7Fu) << 7) | ((d & 0x7F00u) << 15);
-  const uint32_t hi = ((d & 0x7F0000u) >> 9) | ((d & 0x7F000000u) >> 1);
-  return make_uint2(__builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, lo) * k256),
-                    __builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, hi) * k256));
-}
-
-// fp16 block scale b (0..3) of a lane's four.
-__device__ __attribute__((always_inline)) inline _Float16 scale_f16(uint2 sc, int b) {
-  const uint32_t w = (b < 2) ? sc.x : sc.y;
-  return __builtin_bit_cast(_Float16, (uint16_t)((b & 1) ? (w >> 16) : (w & 0xFFFFu)));
-}
 
 // W4A4 on 256 x 256 tiles, four wavefronts (one per SIMD) of 128 x 128 =
 // 4 x 4 MFMA tiles of 32 x 32 -- the largest wave tile, which minimises the
@@ -2158,23 +2347,41 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     hipLaunchKernelGGL(k_gemm_mxfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
     return hipGetLastError();
   }
+  const int cus = device_cus();
   if (a_fmt == 1) {
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;
     const int tiles = g.tiles_m * g.tiles_n;
+    // Few tokens: the split-K kernel on 32 x 64 tiles while those number at
+    // most two per CU (measured at the encoder shapes, M = 16 .. 512: 1.2-1.9x
+    // faster than the 64 x 128 kernel where K >= 3072, equal at K = 1024 up
+    // to 256 rows, slower beyond).
+    const int64_t small_tiles = (int64_t)((m + 31) / 32) * ((n + 63) / 64);
+    if (small_tiles <= 2 * cus) return run_splitk<MODE_FP8, 1, 2, 4, 2>(g, st);
     // Too few 256 x 256 tiles to fill the chip: the 64 x 128 kernel's eight
     // times as many workgroups win. Measured crossover (encoder and
     // transformer widths, M = 128 .. 3072): below 3/8 of a tile per CU.
-    if (m <= 128 || 8 * tiles < 3 * device_cus()) return run_fp8<1, 2>(g, st);
-    hipLaunchKernelGGL(k_gemm_fp8_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    if (m <= 128 || 8 * tiles < 3 * cus) return run_fp8<1, 2>(g, st);
+    hipLaunchKernelGGL(k_gemm_fp8_direct, dim3(std::min(tiles, cus)), dim3(256), 0, st, g);
     return hipGetLastError();
   } else if (a_fmt == 2) {
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;
     const int tiles = g.tiles_m * g.tiles_n;
-    // the same choice for W4A4; measured crossover: one tile per 8 CUs
-    if (m <= 128 || 8 * tiles <= device_cus()) return run<MODE_NVFP4, 2, 2, 1, 2>(g, st);
-    hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, device_cus())), dim3(256), 0, st, g);
+    // Below half a round of 256 x 256 tiles the split-K kernel is faster
+    // (measured up to M = 2300 at N = K = 3072: 0.9x the time there, 0.3x at
+    // M = 512). Tile and split: 64 x 96 tiles, four waves, where they fill
+    // the chip with K >= 2048 (the most MFMAs per expanded operand);
+    // 32 x 64 tiles, eight waves, where that leaves CUs idle; 64 x 64 tiles,
+    // four waves, for short reductions (K < 2048).
+    if (m <= 128 || 2 * tiles < cus) {
+      const int kcn = (int)(k >> 7);
+      const int64_t t6496 = (int64_t)((m + 63) / 64) * ((n + 95) / 96);
+      if (kcn < 16) return run_splitk<MODE_NVFP4, 2, 2, 4, 3>(g, st);
+      if (t6496 >= cus - cus / 4) return run_splitk<MODE_NVFP4, 2, 3, 4, 2>(g, st);
+      return run_splitk<MODE_NVFP4, 1, 2, 8, 3>(g, st);
+    }
+    hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, cus)), dim3(256), 0, st, g);
     return hipGetLastError();
   } else {
     const int64_t npan_all = (n + 31) / 32;

@@ -351,14 +351,19 @@ __global__ void __launch_bounds__(256) k_quant_mx(const uint16_t* __restrict__ x
   for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
   am = max(am, (uint32_t)__shfl_xor((int)am, 1));
   am = max(am, (uint32_t)__shfl_xor((int)am, 2));
-  // floor(log2(max)) from the fp32 bits (normal or denormal), then the code
+  // floor(log2(max)) from the fp32 bits (normal or denormal), then the code.
+  // A block holding inf or NaN gets the E8M0 NaN code 255 (its element codes
+  // are then unspecified: r = 0 makes them signed zeros).
   int e = 0;
-  if (am != 0u) {
+  if (am >= 0x7F800000u) {
+    e = 255;
+  } else if (am != 0u) {
     const int ef = (int)(am >> 23);
     const int fl = (ef > 0) ? ef - 127 : (31 - __builtin_clz(am)) - 149;
     e = min(max(fl - (FP4 ? 2 : 8) + 127, 0), 254);
   }
-  const float r = u2f((uint32_t)(254 - e) << 23);  // 2^(127 - e), e <= 252 here
+  // 2^(127 - e); finite bf16 inputs give e <= 252, so this is a normal number
+  const float r = (e == 255) ? 0.0f : u2f((uint32_t)(254 - e) << 23);
   float y[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
@@ -448,7 +453,8 @@ __global__ void __launch_bounds__(256) k_dequant_mx(const uint8_t* __restrict__ 
   const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (u * 8 >= n) return;
   const uint32_t e = sc[u >> 2];
-  const float scale = (e == 0u) ? u2f(0x00400000u) : u2f(e << 23);  // 2^(e - 127)
+  // 2^(e - 127); code 255 is the E8M0 NaN (a block that held inf or NaN)
+  const float scale = (e == 0u) ? u2f(0x00400000u) : (e == 255u) ? __builtin_nanf("") : u2f(e << 23);
   float v[8];
   if (FP4) {
     const uint32_t w = reinterpret_cast<const uint32_t*>(q)[u];

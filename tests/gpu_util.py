@@ -48,20 +48,88 @@ def assert_quant_equal(qt: q.QTensor, x_bits: np.ndarray):
     assert got_s.view(np.uint32) == np.float32(s).view(np.uint32), (got_s, s)
 
 
-def check_linear(y_dev: torch.Tensor, ref: dict, rows=None, cols=None, tol=1e-3):
-    """|y - y_ref| <= tol * sum|a w| everywhere (or at the sampled outputs).
+def order_key(codes: np.ndarray) -> np.ndarray:
+    """E4M3 codes (sign-magnitude) to integers in value order (-0 and +0 equal)."""
+    c = codes.astype(np.int32)
+    mag = c & 0x7F
+    return np.where(c & 0x80, -mag, mag)
 
-    fp32 outputs get exactly that bound. A bf16 output v' = bf16(v) of an
-    fp32 value v within the bound adds the output rounding:
-    |v' - y_ref| <= 2^-9 |v| + |v - y_ref| <= 2^-9 |y_ref| + (1 + 2^-9) tol * b.
+
+def check_codes(codes, ref, r, rows=None, cols=None, tol=1e-3):
+    y, b = ref["y"], ref["b"]
+    e = tol * b * (1 + 2.0 ** -20) + 1e-300
+    lo = oracle.e4m3_encode_array(((y - e) * r).astype(np.float32))
+    hi = oracle.e4m3_encode_array(((y + e) * r).astype(np.float32))
+    got = codes if rows is None else codes[rows, cols]
+    k, klo, khi = order_key(got), order_key(lo), order_key(hi)
+    bad = np.count_nonzero((k < klo) | (k > khi))
+    assert bad == 0, "%d of %d codes outside the contract" % (bad, k.size)
+    # most codes are the unique rounding (the window holds one code)
+    return float(np.mean(klo == khi))
+
+
+# max err / sum|a w| per named workload case, written out at the end of the
+# session when QG_PARITY_LOG names a file (tests/conftest.py)
+MARGINS = {}
+
+
+def bf16_rne(v: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bf16 value, ties to even, in one
+    rounding (no pass through fp32); returned as float64. bf16 keeps 8
+    significant bits, so ulp(v) = 2^(floor(log2 |v|) - 7)."""
+    v = np.asarray(v, dtype=np.float64)
+    out = np.zeros_like(v)
+    nz = (v != 0) & np.isfinite(v)
+    e = np.floor(np.log2(np.abs(v[nz])))
+    # log2 can land one off at exact powers of two: fix the exponent so that
+    # 2^e <= |v| < 2^(e+1)
+    e = np.where(np.abs(v[nz]) < 2.0 ** e, e - 1, e)
+    e = np.where(np.abs(v[nz]) >= 2.0 ** (e + 1), e + 1, e)
+    e = np.maximum(e, -133.0)                           # bf16 subnormal grid below 2^-126
+    ulp = 2.0 ** (np.maximum(e, -126.0) - 7)
+    out[nz] = np.rint(v[nz] / ulp) * ulp                 # exact scaling, rint ties to even
+    out[~np.isfinite(v)] = v[~np.isfinite(v)]
+    return out
+
+
+def check_linear(y_dev: torch.Tensor, ref: dict, rows=None, cols=None, tol=1e-3, literal=True, name=None):
+    """The GEMM accuracy contract against the oracle's exact product y_ref,
+    at every output (or at the sampled ones), with b = sum_k |a w|:
+
+      fp32 output: |y - y_ref| <= tol * b.
+      bf16 output: y must be the round-to-nearest-even bf16 of some value
+        within tol * b of y_ref, i.e. bf16(y_ref - tol b) <= y <=
+        bf16(y_ref + tol b) (rounding is monotone); and, with literal=True,
+        |y - y_ref| <= tol * b itself at every output where the correctly
+        rounded exact product bf16(y_ref) meets that bound. Where it does not
+        (|y_ref| large against b, so that the bf16 rounding alone, up to
+        2^-8 |y|, exceeds tol * b) no bf16 output can meet it; those outputs
+        are counted in the recorded margins.
+    literal=False is for unit cases with few reduction terms, where many
+    outputs sit within a bf16 rounding step of the bound and the GEMM's own
+    fp32 error may legitimately flip the rounding across it.
     """
     y = host(y_dev.float()).astype(np.float64)
     if rows is not None:
         y = y[rows, cols]
-    err = np.abs(y - ref["y"])
-    bound = tol * ref["b"]
+    yr, b = ref["y"], ref["b"]
+    err = np.abs(y - yr)
+    bound = tol * b
+    worst = float(np.max(err / np.maximum(b, 1e-300))) if err.size else 0.0
+    unreachable = 0
     if y_dev.dtype == torch.bfloat16:
-        bound = (1 + 2.0 ** -9) * bound + 2.0 ** -9 * np.abs(ref["y"])
-    worst = float(np.max(err / np.maximum(ref["b"], 1e-300)))
-    assert np.all(err <= bound), "max err / sum|aw| = %.3e" % worst
+        lo, hi = bf16_rne(yr - bound), bf16_rne(yr + bound)
+        nbad = int(np.count_nonzero((y < lo) | (y > hi)))
+        assert nbad == 0, "%d outputs are not a bf16 rounding of a value within the bound (max err/B %.3e)" % (nbad, worst)
+        reach = np.abs(bf16_rne(yr) - yr) <= bound
+        unreachable = int(np.count_nonzero(~reach))
+        if literal:
+            nlit = int(np.count_nonzero(err[reach] > bound[reach]))
+            assert nlit == 0, "%d outputs beyond %.0e sum|aw| (max err/B %.3e)" % (nlit, tol, worst)
+    else:
+        assert np.all(err <= bound), "max err / sum|aw| = %.3e" % worst
+    if name is not None:
+        MARGINS[name] = {"max_err_over_sum_abs_aw": worst, "bound": tol, "outputs_checked": int(err.size),
+                         "dtype": str(y_dev.dtype).replace("torch.", ""),
+                         "outputs_where_bf16_rounding_alone_exceeds_bound": unreachable}
     return worst

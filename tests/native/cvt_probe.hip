@@ -75,6 +75,26 @@ __global__ void k_probe_f16_scale(uint16_t* out) {
   out[2 * t + 1] = __builtin_bit_cast(uint16_t, (_Float16)b[0]);
 }
 
+// The GEMM kernels' E4M3 block-scale decoders on every code: for code c
+// (0..255) placed in byte position b (0..3) of a dword,
+//   f32[4 c + b] = v_cvt_pk_f32_fp8 (hardware, the W4A16 weight-pool kernels),
+//   and, for c < 128 (block scales are magnitudes),
+//   ref[4 c + b] = dec_e4m3_scale (the W4A16 split-K kernel),
+//   h16[4 c + b] = e4m3x4_to_f16x4 (the W4A4 kernels).
+__global__ void k_probe_scale_decoders(float* f32, float* ref, uint16_t* h16) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 256 * 4) return;
+  const uint32_t c = (uint32_t)t >> 2, b = (uint32_t)t & 3u;
+  const uint32_t d = c << (8 * b);
+  const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)d, false), hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)d, true);
+  f32[t] = (b == 0) ? lo[0] : (b == 1) ? lo[1] : (b == 2) ? hi[0] : hi[1];
+  if (c >= 128u) return;
+  ref[t] = dec_e4m3_scale(d >> (8 * b));
+  const uint2 h = e4m3x4_to_f16x4(d);
+  const uint32_t w = (b < 2) ? h.x : h.y;
+  h16[t] = (uint16_t)((b & 1) ? (w >> 16) : (w & 0xFFFFu));
+}
+
 extern "C" int qgp_probe_cvt(int which, unsigned long long* counts, uint32_t* first) {
   // 4096 x 256 = 2^20 threads; the loops above cover exactly [0, 2^32)
   if (which == 0)
@@ -86,5 +106,10 @@ extern "C" int qgp_probe_cvt(int which, unsigned long long* counts, uint32_t* fi
 
 extern "C" int qgp_probe_f16_scale(uint16_t* out) {
   hipLaunchKernelGGL(k_probe_f16_scale, dim3(16), dim3(256), 0, 0, out);
+  return (int)hipGetLastError();
+}
+
+extern "C" int qgp_probe_scale_decoders(float* f32, float* ref, uint16_t* h16) {
+  hipLaunchKernelGGL(k_probe_scale_decoders, dim3(4), dim3(256), 0, 0, f32, ref, h16);
   return (int)hipGetLastError();
 }

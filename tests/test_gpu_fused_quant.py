@@ -10,33 +10,13 @@ import torch
 import oracle
 import paper_2609_21849_amd as q
 import synth
-from gpu_util import DEV, host, log, to_dev_bf16
+from gpu_util import DEV, check_codes, host, log, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
 
 KINDS = {"fp8": (q.QG_FMT_FP8_E4M3, q.QG_FMT_FP8_E4M3), "nvfp4": (q.QG_FMT_NVFP4, q.QG_FMT_NVFP4),
          "w4a16": (q.QG_FMT_BF16, q.QG_FMT_NVFP4), "mxfp4": (q.QG_FMT_MXFP4, q.QG_FMT_MXFP4),
          "mxfp8": (q.QG_FMT_MXFP8, q.QG_FMT_MXFP8)}
-
-
-def order_key(codes: np.ndarray) -> np.ndarray:
-    """E4M3 codes (sign-magnitude) to integers in value order (-0 and +0 equal)."""
-    c = codes.astype(np.int32)
-    mag = c & 0x7F
-    return np.where(c & 0x80, -mag, mag)
-
-
-def check_codes(codes, ref, r, rows=None, cols=None, tol=1e-3):
-    y, b = ref["y"], ref["b"]
-    e = tol * b * (1 + 2.0 ** -20) + 1e-300
-    lo = oracle.e4m3_encode_array(((y - e) * r).astype(np.float32))
-    hi = oracle.e4m3_encode_array(((y + e) * r).astype(np.float32))
-    got = codes if rows is None else codes[rows, cols]
-    k, klo, khi = order_key(got), order_key(lo), order_key(hi)
-    bad = np.count_nonzero((k < klo) | (k > khi))
-    assert bad == 0, "%d of %d codes outside the contract" % (bad, k.size)
-    # most codes are the unique rounding (the window holds one code)
-    return float(np.mean(klo == khi))
 
 
 def run(kind, x, w, s_y):

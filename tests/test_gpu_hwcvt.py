@@ -44,3 +44,35 @@ def test_f16_conversion_of_e2m1_is_exact_at_unit_scale():
     torch.cuda.synchronize()
     o = out.cpu().numpy().view(np.float16).astype(np.float64).reshape(256, 16, 2)
     assert np.array_equal(o[:, :, 0], np.broadcast_to(oracle.e2m1_table(), (256, 16)))
+
+
+def test_block_scale_decoders_on_every_code():
+    """The E4M3 block-scale decoders the GEMM kernels use, on every code and
+    in every byte position, against the oracle's E4M3 table: the hardware
+    v_cvt_pk_f32_fp8 (W4A16 weight-pool kernels) on all 256 codes (the two
+    NaN codes give NaN), and on the 128 non-negative codes (block scales are
+    magnitudes) the bit-move decoders of the split-K W4A16 kernel (fp32) and
+    of the W4A4 kernels (fp16, four per dword). The E4M3 subnormal codes 1..7
+    become fp32 and fp16 subnormals on the way, so this pins the denormal
+    handling too."""
+    L = _probe()
+    f32 = torch.full((1024,), 12345.0, dtype=torch.float32, device="cuda")
+    ref = torch.full((1024,), 12345.0, dtype=torch.float32, device="cuda")
+    h16 = torch.zeros(1024, dtype=torch.int16, device="cuda")
+    assert L.qgp_probe_scale_decoders(ctypes.c_void_p(f32.data_ptr()), ctypes.c_void_p(ref.data_ptr()),
+                                      ctypes.c_void_p(h16.data_ptr())) == 0
+    torch.cuda.synchronize()
+    table = oracle.e4m3_table()
+    hw = f32.cpu().numpy().astype(np.float64).reshape(256, 4)
+    want = np.broadcast_to(table[:, None], (256, 4))
+    nan = np.isnan(want)
+    assert nan.sum() == 8                                   # 0x7F and 0xFF in four positions
+    assert np.array_equal(np.isnan(hw), nan)
+    assert np.array_equal(hw[~nan], want[~nan])
+    assert np.array_equal(np.signbit(hw[~nan]), np.signbit(want[~nan]))
+    pos = table[:128]
+    assert np.array_equal(ref.cpu().numpy().astype(np.float64).reshape(256, 4)[:127],
+                          np.broadcast_to(pos[:127, None], (127, 4)))
+    h = h16.cpu().numpy().view(np.float16).astype(np.float64)
+    assert np.array_equal(h[:508].reshape(127, 4), np.broadcast_to(pos[:127, None], (127, 4)))
+    assert (pos[1:8] < 2.0 ** -6).all()                     # the subnormal codes are among them

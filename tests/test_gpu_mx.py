@@ -161,7 +161,7 @@ def test_mx_gemm_small_full_parity(fmt, m, n, k, out):
     x = synth.normal_bf16(m, k, 1.0, 11, 0)
     w = synth.normal_bf16(n, k, 0.02, 11, 1)
     y = run_mx_linear(x, w, out, fmt=fmt)
-    log("  max err/B", check_linear(y, oracle.linear_reference(NAME[fmt], x, w)))
+    log("  max err/B", check_linear(y, oracle.linear_reference(NAME[fmt], x, w), literal=False))
 
 
 @pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
@@ -210,4 +210,38 @@ def test_mx_dit_linear_sampled(fmt, name):
     y = run_mx_linear(x, w, fmt=fmt)
     rows, cols = _sample(m, n, 3000, 1)
     ref = oracle.linear_reference(NAME[fmt], x, w, rows=rows, cols=cols)
-    log("  max err/B", check_linear(y, ref, rows, cols))
+    log("  max err/B", check_linear(y, ref, rows, cols,
+                                    name="%s %s %dx%dx%d heavy-tailed (%d sampled)" % (NAME[fmt], name, m, n, k, rows.size)))
+
+
+@pytest.mark.parametrize("fmt", [MXFP4, MXFP8])
+def test_mx_nonfinite_block_gets_nan_scale(fmt):
+    """A block holding inf and a block holding NaN get the E8M0 NaN code 255
+    and decode to NaN; every other block (MX has no tensor-wide reduction) is
+    coded exactly as the oracle codes the same tensor with those two blocks
+    zeroed (the oracle refuses non-finite input)."""
+    rows, cols = 8, 256
+    x = synth.normal_bf16(rows, cols, 1.0, 14, 0)
+    x[2, 37] = 0x7F80          # +inf in block 1 of row 2
+    x[5, 200] = 0xFFC1         # a NaN in block 6 of row 5
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    d = q.dequantize(qt, q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    sc = host(qt.block_scales)
+    assert sc[2, 1] == 255 and sc[5, 6] == 255
+    clean = x.copy()
+    clean[2, 32:64] = 0
+    clean[5, 192:224] = 0
+    codes_ref, sc_ref = oracle.quantize_mx(clean, NAME[fmt])
+    bad = np.zeros(sc_ref.shape, bool)
+    bad[2, 1] = bad[5, 6] = True
+    assert np.array_equal(sc[~bad], sc_ref[~bad])
+    per = 16 if fmt == MXFP4 else 32                       # code bytes per block
+    got = host(qt.codes).reshape(rows, cols // 32, per)
+    want = codes_ref.reshape(rows, cols // 32, per)
+    assert np.array_equal(got[~bad], want[~bad])
+    dv = host(d)
+    assert np.isnan(dv[2, 32:64]).all() and np.isnan(dv[5, 192:224]).all()
+    ok = np.ones(dv.shape, bool)
+    ok[2, 32:64] = ok[5, 192:224] = False
+    assert np.isfinite(dv[ok]).all()

@@ -3,15 +3,19 @@ pinned host memory into device slots on a copy stream, overlapped with the
 GEMMs. Only where the weight bytes come from changes, so every output must be
 bit-identical to the run with all weights resident (the paper's claim for
 streaming, Sec. 4, weight-streaming paragraph), for any slot count, any
-resident subset and across consecutive steps."""
+resident subset and across consecutive steps. The resident run itself is
+checked against the CPU oracle (every output of every layer within
+|y - y_ref| <= 1e-3 sum|a w|), so the streamed runs are tied to the oracle,
+not only to another run of the same kernels."""
 import ctypes
 
 import pytest
 import torch
 
+import oracle
 import paper_2609_21849_amd as q
 import synth
-from gpu_util import DEV, log, to_dev_bf16
+from gpu_util import DEV, check_linear, log, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -26,9 +30,12 @@ LAYERS = [(FP8, FP8, 256, 512, 768, q.QG_OUT_BF16), (NV, NV, 200, 768, 512, q.QG
 class Model:
     def __init__(self):
         self.x, self.codes, self.bs, self.ts, self.wdev, self.whost, self.y = [], [], [], [], [], [], []
+        self.x_bits, self.w_bits = [], []
         for i, (af, wf, m, n, k, od) in enumerate(LAYERS):
-            x = to_dev_bf16(synth.normal_bf16(m, k, 1.0, 40 + i, 0))
-            w = to_dev_bf16(synth.normal_bf16(n, k, 0.02, 40 + i, 1))
+            self.x_bits.append(synth.normal_bf16(m, k, 1.0, 40 + i, 0))
+            self.w_bits.append(synth.normal_bf16(n, k, 0.02, 40 + i, 1))
+            x = to_dev_bf16(self.x_bits[-1])
+            w = to_dev_bf16(self.w_bits[-1])
             packed = q.pack(q.quantize(w, wf))
             host = torch.empty(packed.numel(), dtype=torch.uint8, pin_memory=True)
             host.copy_(packed)
@@ -91,6 +98,12 @@ def reference(model):
         y = q.linear(a, model.wdev[i], wf, n, out_dtype=od)
         torch.cuda.synchronize()
         assert torch.equal(y, ref[i]), i
+    # and every output of the resident run against the oracle
+    kinds = {(FP8, FP8): "fp8", (NV, NV): "nvfp4", (BF16, NV): "w4a16", (MX, MX): "mxfp4"}
+    for i, (af, wf, m, n, k, od) in enumerate(LAYERS):
+        r = oracle.linear_reference(kinds[(af, wf)], model.x_bits[i], model.w_bits[i])
+        worst = check_linear(ref[i], r, name="streaming layer %d %s %dx%dx%d (every output)" % (i, kinds[(af, wf)], m, n, k))
+        log("streaming layer %d %s %dx%dx%d max err/B %.3e" % (i, kinds[(af, wf)], m, n, k, worst))
     return ref
 
 

@@ -634,8 +634,44 @@ def block_chain_part(q, dit, M, steps=10):
                    approximate="tanh")
         return q.linear(q.quantize(u, FP8, static_scale=cal["u"]), by["mlp_down"]["w_fp8"], FP8, 3072)
 
+    # the same with NVFP4: calibrated tensor scales, the QKV and attention-out
+    # outputs written as NVFP4 codes and block scales by their epilogues
+    # (qg_gemm_quant_nvfp4), attention-out reading the V third in place
+    NV = q.QG_FMT_NVFP4
+
+    def calibrate_nv():
+        sc = {}
+        a0 = q.quantize(x0, NV)
+        h = q.linear(a0, by["qkv"]["w_nvfp4"], NV, 9216)
+        av = q.quantize(h[:, 6144:9216], NV)
+        a = q.linear(av, by["attn_out"]["w_nvfp4"], NV, 3072)
+        aa = q.quantize(a, NV)
+        u = F.gelu(q.linear(aa, by["mlp_up"]["w_nvfp4"], NV, 9216), approximate="tanh")
+        au = q.quantize(u, NV)
+        for key, t in (("x0", a0), ("v", av), ("a", aa), ("u", au)):
+            sc[key] = t.tensor_scale.clone()
+        return sc
+
+    cal_nv = calibrate_nv()
+    qkv_nv = (torch.empty((M, 9216 // 2), dtype=torch.uint8, device="cuda"),
+              torch.empty((M, 9216 // 16), dtype=torch.uint8, device="cuda"))
+    ao_nv = (torch.empty((M, 3072 // 2), dtype=torch.uint8, device="cuda"),
+             torch.empty((M, 3072 // 16), dtype=torch.uint8, device="cuda"))
+
+    def chain_nvfp4_fused():
+        a0 = q.quantize(x0, NV, static_scale=cal_nv["x0"])
+        wq, wa = by["qkv"]["w_nvfp4"], by["attn_out"]["w_nvfp4"]
+        q.qg_gemm_quant_nvfp4(NV, a0.codes, a0.block_scales, a0.tensor_scale, 3072, NV, wq, wq.numel(), M, 9216,
+                              3072, qkv_nv[0], qkv_nv[1], 9216, cal_nv["v"])
+        # the V third of the QKV codes and block scales (row pitch 9216 elements)
+        q.qg_gemm_quant_nvfp4(NV, qkv_nv[0].data_ptr() + 3072, qkv_nv[1].data_ptr() + 384, cal_nv["v"], 9216, NV,
+                              wa, wa.numel(), M, 3072, 3072, ao_nv[0], ao_nv[1], 3072, cal_nv["a"])
+        u = F.gelu(q.linear(q.QTensor(NV, ao_nv[0], ao_nv[1], cal_nv["a"], M, 3072), by["mlp_up"]["w_nvfp4"], NV,
+                            9216), approximate="tanh")
+        return q.linear(q.quantize(u, NV, static_scale=cal_nv["u"]), by["mlp_down"]["w_nvfp4"], NV, 3072)
+
     runs = {"bf16": chain_bf16, "fp8": lambda: chain_q("fp8", q.QG_FMT_FP8_E4M3),
-            "fp8_static_fused": chain_fp8_fused,
+            "fp8_static_fused": chain_fp8_fused, "nvfp4_static_fused": chain_nvfp4_fused,
             "nvfp4": lambda: chain_q("nvfp4", q.QG_FMT_NVFP4),
             "mxfp4": lambda: chain_q("mxfp4", q.QG_FMT_MXFP4),
             "mxfp8": lambda: chain_q("mxfp8", q.QG_FMT_MXFP8)}
@@ -652,16 +688,19 @@ def block_chain_part(q, dit, M, steps=10):
         s1.record()
         torch.cuda.synchronize()
         res[name] = {"ms": round(s0.elapsed_time(s1) / steps, 4)}
-    for name in ("fp8", "fp8_static_fused", "nvfp4", "mxfp4", "mxfp8"):
+    for name in ("fp8", "fp8_static_fused", "nvfp4", "nvfp4_static_fused", "mxfp4", "mxfp8"):
         res[name]["speedup_vs_bf16"] = round(res["bf16"]["ms"] / res[name]["ms"], 3)
         # agreement of the chain output with the BF16 chain (relative Frobenius error)
         d = (outs[name].float() - outs["bf16"].float()).norm() / outs["bf16"].float().norm()
         res[name]["rel_err_vs_bf16"] = round(float(d), 4)
     d = (outs["fp8_static_fused"].float() - outs["fp8"].float()).norm() / outs["fp8"].float().norm()
     res["fp8_static_fused"]["rel_diff_vs_fp8_chain"] = round(float(d), 4)
+    d = (outs["nvfp4_static_fused"].float() - outs["nvfp4"].float()).norm() / outs["nvfp4"].float().norm()
+    res["nvfp4_static_fused"]["rel_diff_vs_nvfp4_chain"] = round(float(d), 4)
     res["note"] = ("chain time includes the activation quantizers, GELU and the allocating Python "
-                   "helpers; attention is stubbed; fp8_static_fused: calibrated activation scales, the QKV "
-                   "and attention-out outputs quantized in their GEMM epilogues (qg_gemm_quant)")
+                   "helpers; attention is stubbed; *_static_fused: calibrated activation scales, the QKV "
+                   "and attention-out outputs quantized in their GEMM epilogues (qg_gemm_quant for FP8, "
+                   "qg_gemm_quant_nvfp4 for NVFP4), attention-out reading the V third of the codes in place")
     return res
 
 

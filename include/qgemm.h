@@ -194,7 +194,10 @@ qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_byt
  *
  * Supported (a_fmt, w_fmt) pairs, else QG_ERR_UNSUPPORTED:
  *   (FP8_E4M3, FP8_E4M3)  W8A8:  a = codes [m, k] (lda = k), a_block_scales NULL
- *   (NVFP4,    NVFP4)     W4A4:  a = codes [m, k/2], a_block_scales [m, k/16] (lda = k)
+ *   (NVFP4,    NVFP4)     W4A4:  a = codes, rows of lda/2 bytes, and
+ *                         a_block_scales, rows of lda/16 bytes (8-byte
+ *                         aligned); lda >= k, lda % 128 == 0 (lda > k reads
+ *                         the first k columns of a wider tensor in place)
  *   (BF16,     NVFP4)     W4A16: a = bf16 [m, lda], a_block_scales and a_tensor_scale NULL
  *   (MXFP4,    MXFP4)     MX W4A4: a = codes [m, k/2], a_block_scales [m, k/32]
  *                         (8-byte aligned, lda = k), a_tensor_scale NULL;
@@ -244,6 +247,40 @@ qg_status qg_gemm_quant(qg_format a_fmt, const void *a, const void *a_block_scal
                         qg_format w_fmt, const void *w_packed, size_t w_packed_bytes,
                         int64_t m, int64_t n, int64_t k,
                         void *y_codes, int64_t ldy, const float *y_scale, void *stream);
+
+/*
+ * qg_gemm_quant_nvfp4 -- qg_gemm whose epilogue writes the output quantized
+ * to NVFP4 with a static (calibrated) tensor decode scale: the next linear's
+ * 4-bit activation operand, produced without the bf16 round trip through
+ * memory and without the three quantize kernels. Paper: Sec. 4, quantization
+ * paragraph (NVFP4 activations for the low-precision linears; PTQ with
+ * calibrated ranges).
+ *   a_fmt ... k     as for qg_gemm; every pair but the weight-only one
+ *                   (BF16, NVFP4), which returns QG_ERR_UNSUPPORTED.
+ *   y_codes         out: rows of ldy/2 bytes, two E2M1 codes per byte
+ *                   (element 2i in the low nibble); 4-byte aligned.
+ *   y_block_scales  out: rows of ldy/16 bytes, one E4M3 scale per 16
+ *                   consecutive elements of a row.
+ *   ldy             elements between rows, >= n, ldy % 16 == 0 (as a W4A4
+ *                   activation operand of a later qg_gemm, the rows then
+ *                   need lda = ldy % 128 == 0, or ldy = n dense).
+ *   y_tensor_scale  in: device fp32 tensor decode scale s_t of the output,
+ *                   0 or >= 2^-96 (e.g. the scale qg_quantize_act derived for
+ *                   calibration data); not written.
+ * Result: the static NVFP4 quantization (qg_quantize_act_static) of the fp32
+ * values y[i,j] that qg_gemm would round to its output type: per 16-block of
+ * a row, s_b = E4M3(fl(max|y| / fl(6 s_t))), S = fl(e4m3(s_b) s_t),
+ * r = S > 0 ? fl(1/S) : 0, q = E2M1(fl(y r)) (round to nearest even,
+ * saturating). With the accuracy contract of qg_gemm, every block scale and
+ * code is a correct rounding for some output within that contract's error of
+ * the exact product.
+ */
+qg_status qg_gemm_quant_nvfp4(qg_format a_fmt, const void *a, const void *a_block_scales,
+                              const float *a_tensor_scale, int64_t lda,
+                              qg_format w_fmt, const void *w_packed, size_t w_packed_bytes,
+                              int64_t m, int64_t n, int64_t k,
+                              void *y_codes, void *y_block_scales, int64_t ldy,
+                              const float *y_tensor_scale, void *stream);
 
 /*
  * qg_dequant -- decode a quantized tensor to bf16 or fp32.

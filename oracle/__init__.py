@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.qo_quantize_fp8_static.argtypes = [P, I64, I64, I64, ctypes.c_float, P]
         L.qo_quantize_nvfp4_static.restype = ctypes.c_int
         L.qo_quantize_nvfp4_static.argtypes = [P, I64, I64, I64, ctypes.c_float, P, P]
+        L.qo_quantize_nvfp4_static_f32.restype = ctypes.c_int
+        L.qo_quantize_nvfp4_static_f32.argtypes = [P, I64, I64, I64, ctypes.c_float, P, P]
         L.qo_dequant_fp8_f64.argtypes = [P, I64, ctypes.c_float, P]
         L.qo_dequant_nvfp4_f64.argtypes = [P, P, I64, I64, ctypes.c_float, P]
         L.qo_dequant_fp8_f32.argtypes = [P, I64, ctypes.c_float, P]
@@ -278,6 +280,25 @@ def quantize_nvfp4_static(x_bf16: np.ndarray, s_t):
     codes = np.empty((r, k // 2), dtype=np.uint8)
     bs = np.empty((r, k // 16), dtype=np.uint8)
     st = lib().qo_quantize_nvfp4_static(_ptr(x), r, k, k, float(np.float32(s_t)), _ptr(codes), _ptr(bs))
+    if st == 6:
+        raise NonFiniteInput("tensor holds inf or NaN")
+    if st == 1:
+        raise ValueError("scale must be 0 or at least 2^-96")
+    assert st == 0, st
+    return codes, bs
+
+
+def quantize_nvfp4_static_f32(y_f32: np.ndarray, s_t):
+    """fp32 values [R, K] (a GEMM's fp32 output) and a static tensor decode
+    scale s_t -> (codes uint8 [R, K/2], block scales uint8 [R, K/16]): the
+    static NVFP4 steps on fp32 inputs."""
+    y = _c(y_f32, np.float32)
+    r, k = y.shape
+    if k % 16:
+        raise ValueError("NVFP4 needs K % 16 == 0")
+    codes = np.empty((r, k // 2), dtype=np.uint8)
+    bs = np.empty((r, k // 16), dtype=np.uint8)
+    st = lib().qo_quantize_nvfp4_static_f32(_ptr(y), r, k, k, float(np.float32(s_t)), _ptr(codes), _ptr(bs))
     if st == 6:
         raise NonFiniteInput("tensor holds inf or NaN")
     if st == 1:

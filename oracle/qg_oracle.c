@@ -319,6 +319,52 @@ int qo_quantize_nvfp4_static(const uint16_t *x, int64_t rows, int64_t cols, int6
     return QO_OK;
 }
 
+/*
+ * The same block and element steps on fp32 values with a static tensor
+ * decode scale: the NVFP4 quantization of a GEMM's fp32 output (before any
+ * rounding to bf16), which a fused epilogue performs to hand the next
+ * linear its 4-bit activation. Identical to quantize_nvfp4_core except
+ * that the element values are read as fp32 (a bf16 value widened to fp32
+ * gives the same codes). s_t must be 0 or at least 2^-96; inputs finite.
+ */
+int qo_quantize_nvfp4_static_f32(const float *x, int64_t rows, int64_t cols, int64_t ldx,
+                                 float s_t, uint8_t *codes, uint8_t *block_scales)
+{
+    float d_t;
+    if (cols % 16 != 0)
+        return QO_ERR_SHAPE;
+    if (!scale_ok(s_t, 0x1p-96f))
+        return QO_ERR_INVALID;
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t k = 0; k < cols; ++k)
+            if (!isfinite(x[i * ldx + k]))
+                return QO_ERR_NONFINITE;
+    d_t = 6.0f * s_t;
+    for (int64_t i = 0; i < rows; ++i) {
+        for (int64_t b = 0; b < cols / 16; ++b) {
+            const float *xb = x + i * ldx + b * 16;
+            float a_b = 0.0f, v_b, S, r;
+            uint8_t s_b;
+            for (int t = 0; t < 16; ++t) {
+                float v = fabsf(xb[t]);
+                if (v > a_b)
+                    a_b = v;
+            }
+            v_b = (d_t > 0.0f) ? a_b / d_t : 0.0f;
+            s_b = qo_e4m3_encode(v_b);
+            S = (float)qo_e4m3_value(s_b) * s_t;
+            r = (S > 0.0f) ? 1.0f / S : 0.0f;
+            block_scales[i * (cols / 16) + b] = s_b;
+            for (int t = 0; t < 16; t += 2) {
+                uint8_t lo = qo_e2m1_encode(xb[t] * r);
+                uint8_t hi = qo_e2m1_encode(xb[t + 1] * r);
+                codes[i * (cols / 2) + b * 8 + t / 2] = (uint8_t)(lo | (hi << 4));
+            }
+        }
+    }
+    return QO_OK;
+}
+
 /* ------------------------------------------------------------------ */
 /* MX formats (OCP Microscaling v1.0): the matrix-core-native block    */
 /* scaling of gfx950, a variant beside the paper's NVFP4               */

@@ -25,7 +25,7 @@ QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
                 4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
 EXPORTS = ["qg_quantize_act", "qg_quantize_act_static", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
-           "qg_gemm_quant", "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
+           "qg_gemm_quant", "qg_gemm_quant_nvfp4", "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
            "qg_last_hip_error", "qg_abi_version"]
 
 
@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.qg_gemm.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, I32, P]
         L.qg_gemm_quant.restype = I32
         L.qg_gemm_quant.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, P, P]
+        L.qg_gemm_quant_nvfp4.restype = I32
+        L.qg_gemm_quant_nvfp4.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, P, I64, P, P]
         L.qg_dequant.restype = I32
         L.qg_dequant.argtypes = [I32, P, P, P, I64, I64, P, I32, P]
         D, U8 = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_uint8)
@@ -210,6 +212,30 @@ def qg_gemm_quant(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed
     if check:
         _check(s, "qg_gemm_quant")
     return s
+
+
+def qg_gemm_quant_nvfp4(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_packed_bytes, m, n, k,
+                        y_codes, y_block_scales, ldy, y_tensor_scale, stream=None, check=True):
+    s = lib().qg_gemm_quant_nvfp4(a_fmt, _p(a), _p(a_block_scales), _p(a_tensor_scale), lda, w_fmt, _p(w_packed),
+                                  w_packed_bytes, m, n, k, _p(y_codes), _p(y_block_scales), ldy,
+                                  _p(y_tensor_scale), _stream(stream))
+    if check:
+        _check(s, "qg_gemm_quant_nvfp4")
+    return s
+
+
+def linear_nvfp4_out(a, w_packed, w_fmt: int, n: int, y_tensor_scale, stream=None) -> "QTensor":
+    """Y = A . W^T written as NVFP4 codes and E4M3 block scales with the static
+    tensor decode scale y_tensor_scale (a one-element fp32 CUDA tensor): the
+    next linear's 4-bit activation."""
+    import torch
+    m, k, a_fmt, a_data, a_bs, a_ts, lda, dev = _operands(a, w_packed)
+    _need(y_tensor_scale, "y_tensor_scale", torch.float32, None, dev)
+    codes = torch.empty((m, n // 2), dtype=torch.uint8, device=dev)
+    bs = torch.empty((m, n // 16), dtype=torch.uint8, device=dev)
+    qg_gemm_quant_nvfp4(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, codes, bs, n,
+                        y_tensor_scale, stream)
+    return QTensor(QG_FMT_NVFP4, codes, bs, y_tensor_scale, m, n)
 
 
 def linear_fp8_out(a, w_packed, w_fmt: int, n: int, y_scale, stream=None) -> "QTensor":

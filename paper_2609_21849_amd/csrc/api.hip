@@ -91,7 +91,7 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
   if (m > 0 && k > 0) {
     const int64_t esz2 = (w8a8 || mx8) ? 2 : ((w4a4 || mx4) ? 1 : 4);  // element size x 2
     const int64_t a_extent = ((m - 1) * lda + k) * esz2 / 2;
-    if (a_extent > kMaxDim || (w4a4 && m * (k / 16) > kMaxDim)) return QG_ERR_SHAPE;
+    if (a_extent > kMaxDim || (w4a4 && m * (lda / 16) > kMaxDim)) return QG_ERR_SHAPE;
   }
   if (packed_total_bytes((int)w_fmt, n, k) > kMaxDim) return QG_ERR_SHAPE;
   if (m > 0 && n > 0) {
@@ -100,7 +100,9 @@ qg_status check_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
       if (a == nullptr) return QG_ERR_INVALID_ARG;
       if (w8a8 && (!aligned(a, 16) || lda % 16 != 0 || a_tensor_scale == nullptr || a_block_scales != nullptr))
         return QG_ERR_INVALID_ARG;
-      if (w4a4 && (!aligned(a, 16) || lda != k || a_tensor_scale == nullptr || a_block_scales == nullptr ||
+      // NVFP4 activations: rows of lda / 2 code bytes and lda / 16 scale bytes
+      // (lda > k reads the first k columns of a wider tensor in place)
+      if (w4a4 && (!aligned(a, 16) || lda % 128 != 0 || a_tensor_scale == nullptr || a_block_scales == nullptr ||
                    !aligned(a_block_scales, 8)))
         return QG_ERR_INVALID_ARG;
       if (w4a16 && (!aligned(a, 16) || lda % 8 != 0 || a_tensor_scale != nullptr || a_block_scales != nullptr))
@@ -266,7 +268,7 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
     if (c != QG_OK) return c;
     return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
                                       a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
-                                      n, k, y, ldy, y_dtype == QG_OUT_F32 ? 1 : 0, nullptr,
+                                      n, k, y, ldy, y_dtype == QG_OUT_F32 ? 1 : 0, nullptr, nullptr,
                                       reinterpret_cast<hipStream_t>(stream)));
   }();
   if (qg::log_enabled())
@@ -286,10 +288,37 @@ qg_status qg_gemm_quant(qg_format a_fmt, const void* a, const void* a_block_scal
     if (c != QG_OK) return c;
     return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
                                       a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
-                                      n, k, y_codes, ldy, 2, y_scale, reinterpret_cast<hipStream_t>(stream)));
+                                      n, k, y_codes, ldy, 2, y_scale, nullptr, reinterpret_cast<hipStream_t>(stream)));
   }();
   if (qg::log_enabled())
     qg::log_call("qg_gemm_quant", st_, "a_fmt=%d w_fmt=%d m=%lld n=%lld k=%lld lda=%lld ldy=%lld",
+                 (int)a_fmt, (int)w_fmt, (long long)m, (long long)n, (long long)k, (long long)lda,
+                 (long long)ldy);
+  return st_;
+}
+
+qg_status qg_gemm_quant_nvfp4(qg_format a_fmt, const void* a, const void* a_block_scales,
+                              const float* a_tensor_scale, int64_t lda, qg_format w_fmt, const void* w_packed,
+                              size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y_codes,
+                              void* y_block_scales, int64_t ldy, const float* y_tensor_scale, void* stream) {
+  const qg_status st_ = [&]() -> qg_status {
+    if (y_tensor_scale == nullptr || !aligned(y_tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+    // codes are written four bytes at a time, rows of ldy / 2 bytes
+    const qg_status c = qg::check_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed,
+                                       w_packed_bytes, m, n, k, y_codes, ldy, 4);
+    if (c != QG_OK) return c;
+    if (a_fmt == QG_FMT_BF16) return QG_ERR_UNSUPPORTED;  // weight-only linears keep bf16 / fp32 outputs
+    if (m > 0 && ldy % 16 != 0) return QG_ERR_INVALID_ARG;
+    if (m > 0 && n > 0 && (y_block_scales == nullptr || !aligned(y_codes, 4))) return QG_ERR_INVALID_ARG;
+    if (m > 0 && ((m - 1) * ldy + n) / 2 > kMaxDim) return QG_ERR_SHAPE;
+    return hip_status(qg::launch_gemm((int)a_fmt, a, reinterpret_cast<const uint8_t*>(a_block_scales),
+                                      a_tensor_scale, lda, reinterpret_cast<const uint8_t*>(w_packed), m,
+                                      n, k, y_codes, ldy, 3, y_tensor_scale,
+                                      reinterpret_cast<uint8_t*>(y_block_scales),
+                                      reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_gemm_quant_nvfp4", st_, "a_fmt=%d w_fmt=%d m=%lld n=%lld k=%lld lda=%lld ldy=%lld",
                  (int)a_fmt, (int)w_fmt, (long long)m, (long long)n, (long long)k, (long long)lda,
                  (long long)ldy);
   return st_;

@@ -66,12 +66,13 @@ struct GemmArgs {
   int m, n, k;
   void* y;
   int64_t ldy;
-  int out_mode;             // OUT_BF16, OUT_F32 or OUT_FP8 (E4M3 codes, static scale)
-  const float* y_scale;     // decode scale of the FP8 output
+  int out_mode;             // OUT_BF16, OUT_F32, OUT_FP8 or OUT_NVFP4 (static output scale)
+  const float* y_scale;     // decode scale of the FP8 output / tensor scale of the NVFP4 output
+  uint8_t* y_bscale;        // NVFP4 output: E4M3 block scales [m, ldy / 16]
   int tiles_m, tiles_n;
 };
 
-constexpr int OUT_BF16 = 0, OUT_F32 = 1, OUT_FP8 = 2;
+constexpr int OUT_BF16 = 0, OUT_F32 = 1, OUT_FP8 = 2, OUT_NVFP4 = 3;
 
 // Cache-policy operand of a buffer load: non-temporal, for data that one call
 // reads exactly once (a streamed weight pool).
@@ -120,6 +121,73 @@ __device__ __attribute__((always_inline)) inline void store4(const GemmArgs& g, 
 __device__ __attribute__((always_inline)) inline bool out_vec(const GemmArgs& g) {
   const int esz = g.out_mode == OUT_F32 ? 4 : g.out_mode == OUT_FP8 ? 1 : 2;
   return ((reinterpret_cast<uintptr_t>(g.y) & (4 * esz - 1)) == 0) && ((g.ldy & 3) == 0);
+}
+
+// NVFP4 output (qg_gemm_quant_nvfp4): the static NVFP4 quantizer's steps on
+// the fp32 output values y (the values store4 would round), with the
+// output's tensor decode scale s_t: d = fl(6 s_t); per 16-block of a row
+// v = d > 0 ? fl(max|y| / d) : 0, s_b = E4M3(v) (saturating at 448),
+// S = fl(e4m3(s_b) s_t), r = S > 0 ? fl(1/S) : 0, q = E2M1(fl(y r)). Codes
+// two per byte (element 2i in the low nibble), rows of ldy / 2 bytes; block
+// scales one byte per block, rows of ldy / 16 bytes.
+__device__ __attribute__((always_inline)) inline float nv_out_d(const GemmArgs& g) {
+  return g.out_mode == OUT_NVFP4 ? __fmul_rn(6.0f, *g.y_scale) : 0.0f;
+}
+
+// E4M3 block scale of a block whose largest |y| has the bit pattern amax,
+// and the reciprocal r its elements are multiplied by.
+__device__ __attribute__((always_inline)) inline uint32_t nv_block(uint32_t amax, float st, float d, float& r) {
+  const float vb = (d > 0.0f) ? __fdiv_rn(u2f(amax), d) : 0.0f;
+  const uint32_t sb = enc_e4m3(vb);
+  const float S = __fmul_rn(dec_e4m3(sb), st);
+  r = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
+  return sb;
+}
+
+// One 16-block of row m held by a lane pair in the MFMA output layout: lane
+// half g holds columns n16 + 4 g + [0, 4) in v[0..3] and n16 + 8 + 4 g +
+// [0, 4) in v[4..7]. Both lanes of the pair (l, l ^ 32) call this together.
+// Lane half 0 stores bytes 0..3 of the block's codes, half 1 bytes 4..7.
+__device__ __attribute__((always_inline)) inline void store_nv_pair(const GemmArgs& g, int m, int n16,
+                                                                    const float (&v)[8], int gq, float st,
+                                                                    float d) {
+  uint32_t am = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
+  am = max(am, (uint32_t)__shfl_xor((int)am, 32));
+  float r;
+  const uint32_t sb = nv_block(am, st, d, r);
+  float y[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
+  // half 0 holds the bytes of elements 0-3 and 8-11 ([b0 b1 b4 b5]), half 1
+  // those of 4-7 and 12-15 ([b2 b3 b6 b7]); one exchange makes them runs
+  const uint32_t w = hw_e2m1x8(y);
+  const uint32_t x = (uint32_t)__shfl_xor((int)w, 32);
+  const uint32_t out = gq ? ((x >> 16) | (w & 0xFFFF0000u)) : ((w & 0xFFFFu) | (x << 16));
+  uint8_t* row = reinterpret_cast<uint8_t*>(g.y) + (int64_t)m * (g.ldy >> 1);
+  *reinterpret_cast<uint32_t*>(row + (n16 >> 1) + 4 * gq) = out;
+  if (gq == 0) g.y_bscale[(int64_t)m * (g.ldy >> 4) + (n16 >> 4)] = (uint8_t)sb;
+}
+
+// One 16-block of row m held by four consecutive lanes, lane n / 4 % 4
+// holding columns n .. n + 3 in v (the split-K kernels' reduction layout).
+// All four lanes call this together.
+__device__ __attribute__((always_inline)) inline void store_nv_quad(const GemmArgs& g, int m, int n,
+                                                                    const float (&v)[4], float st, float d) {
+  uint32_t am = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
+  am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+  am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+  float r;
+  const uint32_t sb = nv_block(am, st, d, r);
+  uint32_t w = 0;
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, __fmul_rn(v[0], r), __fmul_rn(v[1], r), 1.0f, 0);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, __fmul_rn(v[2], r), __fmul_rn(v[3], r), 1.0f, 1);
+  uint8_t* row = reinterpret_cast<uint8_t*>(g.y) + (int64_t)m * (g.ldy >> 1);
+  *reinterpret_cast<uint16_t*>(row + (n >> 1)) = (uint16_t)w;
+  if ((n & 15) == 0) g.y_bscale[(int64_t)m * (g.ldy >> 4) + (n >> 4)] = (uint8_t)sb;
 }
 
 // LDS bytes per 32-row panel per 128-chunk of the large-M W4A16 kernel:
@@ -408,6 +476,51 @@ __device__ __attribute__((always_inline)) inline __amdgpu_buffer_rsrc_t rsrc_a_f
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)bytes, 0x00020000);
 }
 
+// Epilogue shared by the MFMA-layout kernels: a wave's TM x TN accumulator tiles,
+// first output row mw and column nw, scaled by c and rounded to the output
+// type. Lane l holds Y[mw + 32 i + l % 32][nw + 32 j + 8 q + 4 (l / 32) + e].
+template <int TM, int TN>
+__device__ __attribute__((always_inline)) inline void store_tiles(const GemmArgs& g, const v16f (&acc)[TM][TN],
+                                                                  int mw, int nw, int lane, float c) {
+  if (g.out_mode == OUT_NVFP4) {
+    const float st = *g.y_scale, d = nv_out_d(g);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mw + 32 * i + (lane & 31);
+      if (m >= g.m) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int n16 = nw + 32 * j + 16 * b;
+          if (n16 >= g.n) continue;
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = acc[i][j][8 * b + e] * c;
+          store_nv_pair(g, m, n16, v, lane >> 5, st, d);
+        }
+    }
+    return;
+  }
+  const bool vec = out_vec(g);
+  const float ry = out_rscale(g);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = mw + 32 * i + (lane & 31);
+    if (m >= g.m) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int n = nw + 32 * j + 8 * qd + 4 * (lane >> 5);
+        if (n >= g.n) continue;
+        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
+               acc[i][j][4 * qd + 3] * c, vec, ry);
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- FP8 (W8A8), few tokens
 // Four wavefronts (one per SIMD) on a (64 TM) x (64 TN) tile, each owning
 // TM x TN MFMA tiles of 32 x 32 (used with TM = 1, TN = 2: 64 x 128 tiles,
@@ -552,24 +665,7 @@ __global__ void __launch_bounds__(256) k_gemm_fp8(GemmArgs g) {
     }
   }
 
-  const float c = *g.w_tscale * *g.a_tscale;
-  const bool vec = out_vec(g);
-  const float ry = out_rscale(g);
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int m = m0 + (wm * TM + i) * 32 + (lane & 31);
-    if (m >= g.m) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-#pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const int n = n0 + (wn * TN + j) * 32 + 8 * qd + 4 * gq;
-        if (n >= g.n) continue;
-        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
-               acc[i][j][4 * qd + 3] * c, vec, ry);
-      }
-    }
-  }
+  store_tiles<TM, TN>(g, acc, m0 + wm * TM * 32, n0 + wn * TN * 32, lane, *g.w_tscale * *g.a_tscale);
 }
 
 template <int TM, int TN>
@@ -635,11 +731,16 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * (MODE == MODE_FP8 ? 4096 : 2048)), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_scales), 0, MODE == MODE_NVFP4 ? (int)((int64_t)npanels_w * kcn * 256) : 0, 0x00020000);
+  // NVFP4 activation rows: lda / 2 code bytes and lda / 16 scale bytes apart,
+  // the descriptors ending at the last row's k / 2 and k / 16 bytes
+  const int64_t ka = g.lda >> 1, ks = g.lda >> 4;
   const __amdgpu_buffer_rsrc_t rs_a = (MODE == MODE_FP8)
       ? rsrc_a_fp8(g)
-      : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * (g.k >> 1)), 0x00020000);
+      : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)((int64_t)(g.m - 1) * ka + (g.k >> 1)),
+                                          0x00020000);
   const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(g.a_bscale), 0, MODE == MODE_NVFP4 ? (int)((int64_t)g.m * (g.k >> 4)) : 0, 0x00020000);
+      const_cast<uint8_t*>(g.a_bscale), 0, MODE == MODE_NVFP4 ? (int)((int64_t)(g.m - 1) * ks + (g.k >> 4)) : 0,
+      0x00020000);
 
   // per-lane base offsets (rows and panels outside the operands: out of range, zeros)
   uint32_t oa[MT], oas[MT], ow[NP], ows[NP];
@@ -651,8 +752,8 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
       oa[i] = in ? (uint32_t)((int64_t)row * g.lda + 32 * gq) : OOB;
       oas[i] = OOB;
     } else {
-      oa[i] = in ? (uint32_t)(row * (g.k >> 1) + 32 * gq) : OOB;
-      oas[i] = in ? (uint32_t)(row * (g.k >> 4) + 4 * gq) : OOB;
+      oa[i] = in ? (uint32_t)(row * ka + 32 * gq) : OOB;
+      oas[i] = in ? (uint32_t)(row * ks + 4 * gq) : OOB;
     }
   }
 #pragma unroll
@@ -835,6 +936,9 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   const float c = *g.w_tscale * *g.a_tscale;
   const bool vec = out_vec(g);
   const float ry = out_rscale(g);
+  const bool nv = g.out_mode == OUT_NVFP4;
+  const float st = nv ? *g.y_scale : 0.0f, d = nv_out_d(g);
+  // the four lanes of a 16-block are consecutive (BN / 4 is a multiple of 8)
   for (int u = threadIdx.x; u < BM * (BN / 4); u += 64 * NW) {
     const int row = u / (BN / 4), c4 = u - row * (BN / 4);
     const int m = m0 + row, n = n0 + 4 * c4;
@@ -845,7 +949,12 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
       const float4 v = *reinterpret_cast<const float4*>(red + w * (BM * LDR) + row * LDR + 4 * c4);
       sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
     }
-    store4(g, m, n, sum.x * c, sum.y * c, sum.z * c, sum.w * c, vec, ry);
+    if (nv) {
+      const float v[4] = {sum.x * c, sum.y * c, sum.z * c, sum.w * c};
+      store_nv_quad(g, m, n, v, st, d);
+    } else {
+      store4(g, m, n, sum.x * c, sum.y * c, sum.z * c, sum.w * c, vec, ry);
+    }
   }
 }
 
@@ -858,31 +967,6 @@ static hipError_t run_splitk(GemmArgs g, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------- FP8, 256 x 256 tiles
-// Epilogue shared by the FP8 kernels: a wave's TM x TN accumulator tiles,
-// first output row mw and column nw, scaled by c and rounded to the output
-// type. Lane l holds Y[mw + 32 i + l % 32][nw + 32 j + 8 q + 4 (l / 32) + e].
-template <int TM, int TN>
-__device__ __attribute__((always_inline)) inline void store_tiles(const GemmArgs& g, const v16f (&acc)[TM][TN],
-                                                                  int mw, int nw, int lane, float c) {
-  const bool vec = out_vec(g);
-  const float ry = out_rscale(g);
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int m = mw + 32 * i + (lane & 31);
-    if (m >= g.m) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-#pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const int n = nw + 32 * j + 8 * qd + 4 * (lane >> 5);
-        if (n >= g.n) continue;
-        store4(g, m, n, acc[i][j][4 * qd] * c, acc[i][j][4 * qd + 1] * c, acc[i][j][4 * qd + 2] * c,
-               acc[i][j][4 * qd + 3] * c, vec, ry);
-      }
-    }
-  }
-}
-
 // Epilogue fast path: bf16 output, whole tile inside the output, 16-byte
 // aligned rows. Stored straight from the MFMA layout, every store
 // instruction would scatter 8-byte pieces over 32 rows, which the memory
@@ -1395,11 +1479,13 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   const int total = g.tiles_m * g.tiles_n;
   const float scale = *g.w_tscale * *g.a_tscale;
   const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
-  const uint32_t ka = (uint32_t)(g.k >> 1), ks = (uint32_t)(g.k >> 4);  // A code / scale bytes per row
+  // A rows: lda / 2 code bytes and lda / 16 scale bytes apart; the
+  // descriptors end at the last row's k / 2 and k / 16 bytes
+  const uint32_t ka = (uint32_t)(g.lda >> 1), ks = (uint32_t)(g.lda >> 4);
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(g.a), 0, (int)((int64_t)g.m * ka), 0x00020000);
+      const_cast<uint8_t*>(g.a), 0, (int)((int64_t)(g.m - 1) * ka + (g.k >> 1)), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(g.a_bscale), 0, (int)((int64_t)g.m * ks), 0x00020000);
+      const_cast<uint8_t*>(g.a_bscale), 0, (int)((int64_t)(g.m - 1) * ks + (g.k >> 4)), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 2048), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs_bs = __builtin_amdgcn_make_buffer_rsrc(
@@ -2273,13 +2359,19 @@ __global__ void __launch_bounds__(512, 4) k_w4a16_gemv(GemmArgs g) {
   }
 }
 
-__global__ void k_zero_rows(void* y, int64_t m, int64_t n, int64_t ldy, int out_mode) {
+// k = 0: every output is zero (NVFP4: zero codes and zero block scales, one
+// thread per code byte).
+__global__ void k_zero_rows(void* y, uint8_t* y_bscale, int64_t m, int64_t n, int64_t ldy, int out_mode) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= m * n) return;
-  const int64_t r = t / n, c = t - r * n;
+  const int64_t w = (out_mode == OUT_NVFP4) ? n / 2 : n;  // items per row
+  if (t >= m * w) return;
+  const int64_t r = t / w, c = t - r * w;
   if (out_mode == OUT_F32) reinterpret_cast<float*>(y)[r * ldy + c] = 0.0f;
   else if (out_mode == OUT_FP8) reinterpret_cast<uint8_t*>(y)[r * ldy + c] = 0;
-  else reinterpret_cast<uint16_t*>(y)[r * ldy + c] = 0;
+  else if (out_mode == OUT_NVFP4) {
+    reinterpret_cast<uint8_t*>(y)[r * (ldy / 2) + c] = 0;
+    if (c % 8 == 0) y_bscale[r * (ldy / 16) + c / 8] = 0;
+  } else reinterpret_cast<uint16_t*>(y)[r * ldy + c] = 0;
 }
 
 template <int MODE, int WM, int WN, int TM, int TN, int DEPTH = 1>
@@ -2309,10 +2401,12 @@ static int device_cus() {
 
 hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const float* a_tscale,
                        int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
-                       void* y, int64_t ldy, int out_mode, const float* y_scale, hipStream_t st) {
+                       void* y, int64_t ldy, int out_mode, const float* y_scale, uint8_t* y_bscale,
+                       hipStream_t st) {
   if (m == 0 || n == 0) return hipSuccess;
   if (k == 0) {
-    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, m, n, ldy, out_mode);
+    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, y_bscale, m, n, ldy,
+                       out_mode);
     return hipGetLastError();
   }
   const int w_fmt = (a_fmt == 1 || a_fmt == 3 || a_fmt == 4) ? a_fmt : 2;
@@ -2331,6 +2425,7 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
   g.ldy = ldy;
   g.out_mode = out_mode;
   g.y_scale = y_scale;
+  g.y_bscale = y_bscale;
   g.tiles_m = g.tiles_n = 0;
   // persistent grids of 256 x 256 tiles, four waves of 128 x 128 each
   if (a_fmt == 4) {

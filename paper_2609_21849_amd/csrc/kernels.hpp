@@ -44,9 +44,12 @@ hipError_t launch_pack(int fmt, const uint8_t* codes, const uint8_t* bscale, con
                        int64_t n, int64_t k, uint8_t* packed, hipStream_t st);
 hipError_t launch_unpack(int fmt, const uint8_t* packed, int64_t n, int64_t k, uint8_t* codes,
                          uint8_t* bscale, float* tscale, hipStream_t st);
-// out_mode: 0 bf16, 1 fp32, 2 E4M3 codes of y / *y_scale (y_scale: device fp32)
+// out_mode: 0 bf16, 1 fp32, 2 E4M3 codes of y / *y_scale (y_scale: device
+// fp32), 3 NVFP4 codes [m, ldy / 2] and E4M3 block scales y_bscale
+// [m, ldy / 16] with the static tensor decode scale *y_scale
 hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const float* a_tscale,
                        int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
-                       void* y, int64_t ldy, int out_mode, const float* y_scale, hipStream_t st);
+                       void* y, int64_t ldy, int out_mode, const float* y_scale, uint8_t* y_bscale,
+                       hipStream_t st);
 
 }  // namespace qg

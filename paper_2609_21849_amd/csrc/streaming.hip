@@ -252,7 +252,7 @@ qg_status qg_run_layers(const qg_stream_layer* layers, int32_t n_layers, void* c
       e = qg::launch_gemm((int)L.a_fmt, bf16 ? L.x : L.a_codes,
                           reinterpret_cast<const uint8_t*>(bf16 ? nullptr : L.a_block_scales),
                           bf16 ? nullptr : L.a_tensor_scale, L.k, reinterpret_cast<const uint8_t*>(wdev), L.m, L.n,
-                          L.k, L.y, L.n, L.y_dtype == QG_OUT_F32 ? 1 : 0, nullptr, cs);
+                          L.k, L.y, L.n, L.y_dtype == QG_OUT_F32 ? 1 : 0, nullptr, nullptr, cs);
       if (e != hipSuccess) return qg::status_of(e);
       if (!L.resident && (e = hipEventRecord(free_ev, cs)) != hipSuccess) return qg::status_of(e);
     }

@@ -133,3 +133,57 @@ def check_linear(y_dev: torch.Tensor, ref: dict, rows=None, cols=None, tol=1e-3,
                          "dtype": str(y_dev.dtype).replace("torch.", ""),
                          "outputs_where_bf16_rounding_alone_exceeds_bound": unreachable}
     return worst
+
+
+def _f32_down(x):
+    v = np.asarray(x, dtype=np.float64).astype(np.float32)
+    return np.where(v.astype(np.float64) > x, np.nextafter(v, np.float32(-np.inf)), v).astype(np.float32)
+
+
+def _f32_up(x):
+    v = np.asarray(x, dtype=np.float64).astype(np.float32)
+    return np.where(v.astype(np.float64) < x, np.nextafter(v, np.float32(np.inf)), v).astype(np.float32)
+
+
+def _e2m1_key(c):
+    c = c.astype(np.int32)
+    mag = c & 7
+    return np.where(c & 8, -mag, mag)
+
+
+def check_nvfp4_codes(codes, bscales, ref, s_t, tol=1e-3):
+    """NVFP4 output of a GEMM epilogue against the oracle's exact product
+    y_ref (rows of whole 16-blocks): every block scale and code must be a
+    correct rounding (the static NVFP4 steps in fp32) for some output y' with
+    |y' - y_ref| <= tol * sum|a w| elementwise. Sound bounds: the block scale
+    lies between the scales of the smallest and largest possible block max,
+    and, given the block scale actually chosen, each code lies between the
+    codes of the smallest and largest possible element. Returns the share of
+    blocks whose scale window holds a single code."""
+    y, b = ref["y"], ref["b"]
+    rows, n = y.shape
+    e = tol * b * (1 + 2.0 ** -20) + 1e-300
+    s_t = np.float32(s_t)
+    d = np.float32(np.float32(6.0) * s_t)
+    lo_abs = np.maximum(np.abs(y) - e, 0.0).reshape(rows, n // 16, 16).max(axis=2)
+    hi_abs = (np.abs(y) + e).reshape(rows, n // 16, 16).max(axis=2)
+    if d > 0:
+        v_lo, v_hi = _f32_down(lo_abs) / d, _f32_up(hi_abs) / d
+    else:
+        v_lo = v_hi = np.zeros_like(lo_abs, dtype=np.float32)
+    sb_lo = oracle.e4m3_encode_array(v_lo.astype(np.float32))
+    sb_hi = oracle.e4m3_encode_array(v_hi.astype(np.float32))
+    bad = np.count_nonzero((bscales < sb_lo) | (bscales > sb_hi))
+    assert bad == 0, "%d of %d block scales outside the contract" % (bad, bscales.size)
+    S = (oracle.e4m3_table()[bscales].astype(np.float32) * s_t).astype(np.float32)
+    r = np.where(S > 0, np.float32(1.0) / np.where(S > 0, S, np.float32(1.0)), np.float32(0.0)).astype(np.float32)
+    rr = np.repeat(r, 16, axis=1)
+    c_lo = oracle.e2m1_encode_array((_f32_down(y - e) * rr).astype(np.float32))
+    c_hi = oracle.e2m1_encode_array((_f32_up(y + e) * rr).astype(np.float32))
+    got = np.empty((rows, n), dtype=np.uint8)
+    got[:, 0::2] = codes & 0xF
+    got[:, 1::2] = codes >> 4
+    k, klo, khi = _e2m1_key(got), _e2m1_key(c_lo), _e2m1_key(c_hi)
+    badc = np.count_nonzero((k < klo) | (k > khi))
+    assert badc == 0, "%d of %d codes outside the contract" % (badc, k.size)
+    return float(np.mean(sb_lo == sb_hi))

@@ -133,7 +133,9 @@ def test_gemm_validation():
     assert _gemm(y=None) == INVALID
     assert _gemm(a=None) == INVALID
     assert _gemm(abs_=None) == INVALID                                   # W4A4 needs A block scales
-    assert _gemm(lda=512) == INVALID                                     # W4A4 codes are dense
+    assert _gemm(lda=320) == INVALID                                     # W4A4 row pitch % 128
+    assert _gemm(lda=512) not in (INVALID, SHAPE)                        # a slice of a wider tensor
+    assert _gemm(m=70000, lda=65536) == SHAPE                            # scales + codes above 2 GiB
     assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, a=P + 8) == INVALID     # 16-byte alignment
     # operand extents above 2 GiB (32-bit buffer offsets)
     assert _gemm(a_fmt=FP8, w_fmt=FP8, abs_=None, m=70000, lda=32768, k=32768) == SHAPE
@@ -238,3 +240,22 @@ def test_gemm_quant_validation():
     assert gq(y=None) == INVALID
     assert gq(wbytes=100) == SMALL
     assert gq(ats=None) == INVALID                     # the GEMM's own operand checks
+
+
+def test_gemm_quant_nvfp4_validation():
+    def gq(a_fmt=NVFP4, w_fmt=NVFP4, abs_=P, ats=P, lda=256, y=P, ybs=P, ldy=64, ys=P, m=32, n=64, k=256,
+           wbytes=1 << 24):
+        return q.qg_gemm_quant_nvfp4(a_fmt, P, abs_, ats, lda, w_fmt, P, wbytes, m, n, k, y, ybs, ldy, ys,
+                                     stream=0, check=False)
+    assert gq(ys=None) == INVALID                      # the output's tensor scale is required
+    assert gq(ys=P + 2) == INVALID
+    assert gq(ybs=None) == INVALID                     # block scales out
+    assert gq(y=P + 2) == INVALID                      # 4-byte aligned codes
+    assert gq(ldy=72) == INVALID                       # ldy % 16
+    assert gq(ldy=32) == INVALID                       # ldy < n
+    assert gq(a_fmt=BF16, abs_=None, ats=None) == UNSUP  # weight-only: bf16 / fp32 outputs only
+    assert gq(a_fmt=FP8, w_fmt=NVFP4) == UNSUP
+    assert gq(n=40) == SHAPE
+    assert gq(wbytes=100) == SMALL
+    assert gq(ats=None) == INVALID                     # the GEMM's own operand checks
+    assert gq(m=0) == OK and gq(n=0, ldy=0) == OK      # nothing to do

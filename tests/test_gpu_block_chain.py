@@ -29,7 +29,8 @@ import torch.nn.functional as F
 import oracle
 import paper_2609_21849_amd as q
 import synth
-from gpu_util import DEV, assert_quant_equal, check_codes, check_linear, host, log, scale_of, to_dev_bf16
+from gpu_util import (DEV, assert_quant_equal, check_codes, check_linear, check_nvfp4_codes, host, log, scale_of,
+                      to_dev_bf16)
 
 pytestmark = pytest.mark.gpu
 
@@ -167,3 +168,81 @@ def test_static_fused_chain_each_linear_against_oracle(block):
     ref = _ref_on_codes(au_ref, s["u"], *wq["mlp_down"], rows, cols)
     log("  mlp_down max err/B %.3e" % check_linear(y, ref, rows, cols,
                                                    name="chain fp8 static-fused mlp_down %dx3072x9216 (%d sampled)" % (M, rows.size)))
+
+
+def test_static_fused_nvfp4_chain_each_linear_against_oracle(block):
+    """The NVFP4 chain with calibrated tensor scales: QKV and attention-out
+    write NVFP4 codes and block scales in their epilogues, attention-out
+    reads the V third of the QKV codes in place (row pitch 9216 elements:
+    codes + 3072 bytes, block scales + 384 bytes). Whole sampled rows (the
+    block scales span 16 columns) are held to the NVFP4 rounding window; the
+    next linear is checked on the decoded codes the GPU fed it."""
+    x0, ws, wd = block
+    NV = q.QG_FMT_NVFP4
+    log("block chain nvfp4 static + fused epilogue quantization M=%d" % M)
+    packed = {name: q.pack(q.quantize(wd[name], NV)) for name in ws}
+    wq = {name: oracle.quantize_nvfp4(w) for name, w in ws.items()}
+    xc = to_dev_bf16(synth.normal_bf16(M, 3072, 1.0, 65, 0))
+    c0 = q.quantize(xc, NV)
+    hc = q.linear(c0, packed["qkv"], NV, 9216)
+    cv = q.quantize(hc[:, 6144:9216], NV)
+    ac = q.linear(cv, packed["attn_out"], NV, 3072)
+    ca = q.quantize(ac, NV)
+    uc = F.gelu(q.linear(ca, packed["mlp_up"], NV, 9216), approximate="tanh")
+    cu = q.quantize(uc, NV)
+    torch.cuda.synchronize()
+    cal = {key: t.tensor_scale.clone() for key, t in (("x0", c0), ("v", cv), ("a", ca), ("u", cu))}
+    s = {key: scale_of(t) for key, t in cal.items()}
+
+    a0 = q.quantize(to_dev_bf16(x0), NV, static_scale=cal["x0"])
+    qkv = (torch.empty((M, 4608), dtype=torch.uint8, device=DEV), torch.empty((M, 576), dtype=torch.uint8, device=DEV))
+    q.qg_gemm_quant_nvfp4(NV, a0.codes, a0.block_scales, a0.tensor_scale, 3072, NV, packed["qkv"],
+                          packed["qkv"].numel(), M, 9216, 3072, qkv[0], qkv[1], 9216, cal["v"])
+    ao = (torch.empty((M, 1536), dtype=torch.uint8, device=DEV), torch.empty((M, 192), dtype=torch.uint8, device=DEV))
+    q.qg_gemm_quant_nvfp4(NV, qkv[0].data_ptr() + 3072, qkv[1].data_ptr() + 384, cal["v"], 9216, NV,
+                          packed["attn_out"], packed["attn_out"].numel(), M, 3072, 3072, ao[0], ao[1], 3072, cal["a"])
+    y_up = q.linear(q.QTensor(NV, ao[0], ao[1], cal["a"], M, 3072), packed["mlp_up"], NV, 9216)
+    u = F.gelu(y_up, approximate="tanh")
+    au = q.quantize(u, NV, static_scale=cal["u"])
+    y = q.linear(au, packed["mlp_down"], NV, 3072)
+    torch.cuda.synchronize()
+
+    def ref_rows(a_codes, a_bs, s_a, name, rows):
+        n = synth.DIT_LINEARS[name][0]
+        qw, bw, sw = wq[name]
+        y_ref, b = oracle.gemm_f64(oracle.dequant_nvfp4(a_codes[rows], a_bs[rows], s_a), oracle.dequant_nvfp4(qw, bw, sw))
+        return {"y": y_ref.reshape(rows.size, n), "b": b.reshape(rows.size, n)}
+
+    rng = np.random.default_rng(70)
+    a0c, a0b = oracle.quantize_nvfp4_static(x0, s["x0"])
+    assert np.array_equal(host(a0.codes), a0c) and np.array_equal(host(a0.block_scales), a0b)
+    rows = np.sort(rng.choice(M, 24, replace=False))
+    uniq = check_nvfp4_codes(host(qkv[0])[rows], host(qkv[1])[rows], ref_rows(a0c, a0b, s["x0"], "qkv", rows), s["v"])
+    log("  qkv fused NVFP4 output within the contract (%.3f unique block scales)" % uniq)
+
+    vc = np.ascontiguousarray(host(qkv[0])[:, 3072:4608])
+    vb = np.ascontiguousarray(host(qkv[1])[:, 384:576])
+    rows = np.sort(rng.choice(M, 24, replace=False))
+    uniq = check_nvfp4_codes(host(ao[0])[rows], host(ao[1])[rows], ref_rows(vc, vb, s["v"], "attn_out", rows), s["a"])
+    log("  attn_out (V slice, row pitch 9216) fused NVFP4 output within the contract (%.3f unique)" % uniq)
+
+    rows, cols = sample(9216, 71)
+    aoc, aob = host(ao[0]), host(ao[1])
+    qw, bw, sw = wq["mlp_up"]
+    ur, ri = np.unique(rows, return_inverse=True)
+    uc_, ci = np.unique(cols, return_inverse=True)
+    yr, b = oracle.gemm_f64_sampled(oracle.dequant_nvfp4(aoc[ur], aob[ur], s["a"]),
+                                    oracle.dequant_nvfp4(qw[uc_], bw[uc_], sw), ri, ci)
+    log("  mlp_up max err/B %.3e" % check_linear(y_up, {"y": yr, "b": b}, rows, cols,
+                                                 name="chain nvfp4 static-fused mlp_up %dx9216x3072 (%d sampled)" % (M, rows.size)))
+    u_bits = bits_of(u)
+    auc, aub = oracle.quantize_nvfp4_static(u_bits, s["u"])
+    assert np.array_equal(host(au.codes), auc) and np.array_equal(host(au.block_scales), aub)
+    rows, cols = sample(3072, 72)
+    qw, bw, sw = wq["mlp_down"]
+    ur, ri = np.unique(rows, return_inverse=True)
+    uc_, ci = np.unique(cols, return_inverse=True)
+    yr, b = oracle.gemm_f64_sampled(oracle.dequant_nvfp4(auc[ur], aub[ur], s["u"]),
+                                    oracle.dequant_nvfp4(qw[uc_], bw[uc_], sw), ri, ci)
+    log("  mlp_down max err/B %.3e" % check_linear(y, {"y": yr, "b": b}, rows, cols,
+                                                   name="chain nvfp4 static-fused mlp_down %dx3072x9216 (%d sampled)" % (M, rows.size)))

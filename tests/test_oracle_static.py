@@ -104,3 +104,51 @@ def test_static_scale_validity_boundaries():
     for bad in (2.0 ** -97, np.nextafter(np.float32(2.0 ** -96), np.float32(0))):
         with pytest.raises(ValueError):
             oracle.quantize_nvfp4_static(x, np.float32(bad))
+
+
+# ---------------------------------------------------------------- static NVFP4 on fp32 values
+@pytest.mark.parametrize("seed", [0, 1])
+def test_nvfp4_static_f32_equals_bf16_path_on_bf16_values(seed):
+    # bf16 values widened to fp32 exactly: the fp32 entry point must give the
+    # codes of the (pinned) bf16 entry point, scale for scale
+    x = synth.normal_bf16(33, 256, 1.0, seed, 0, outlier_frac=0.05, outlier_gain=40.0)
+    x[3, :16] = 0
+    x[4, 16:32] &= 0x807F                                  # subnormal-only block
+    xf = synth.bf16_bits_to_f32(x)
+    _, _, s_dyn = oracle.quantize_nvfp4(x)
+    for s in (s_dyn, np.float32(s_dyn * 0.3), np.float32(s_dyn * 3.0), np.float32(0.0)):
+        c1, b1 = oracle.quantize_nvfp4_static(x, s)
+        c2, b2 = oracle.quantize_nvfp4_static_f32(xf, s)
+        assert np.array_equal(c1, c2) and np.array_equal(b1, b2)
+
+
+def test_nvfp4_static_f32_worked_example():
+    # s_t = fl(1/6): d = fl(6 s_t) = 1 and the block max 6 gives v = 6, an
+    # E4M3 value (1.5 x 2^2: code 0x4C), so S = fl(6 s_t) = 1 and r = 1: each
+    # code is E2M1 of the fp32 value itself. The values sit one fp32 ulp on
+    # either side of the E2M1 midpoints (0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5)
+    # or on them (ties to the even code), which bf16 inputs cannot do.
+    y = np.array([6.0, 1.2500001, 1.2499999, -0.2500001, 0.25, 0.7499999, 0.75, 1.75,
+                  2.5, 2.5000002, 3.4999998, 3.5, 4.9999995, 5.0, 5.0000005, -6.0], dtype=np.float32)
+    # codes: 6 -> 7; 1.2500001 -> 1.5 (3); 1.2499999 -> 1 (2); -0.2500001 -> -0.5 (9);
+    # 0.25 tie -> 0 (0); 0.7499999 -> 0.5 (1); 0.75 tie -> 1 (2); 1.75 tie -> 2 (4);
+    # 2.5 tie -> 2 (4); 2.5000002 -> 3 (5); 3.4999998 -> 3 (5); 3.5 tie -> 4 (6);
+    # 4.9999995 -> 4 (6); 5 tie -> 4 (6); 5.0000005 -> 6 (7); -6 -> -6 (15)
+    want = [7, 3, 2, 9, 0, 1, 2, 4, 4, 5, 5, 6, 6, 6, 7, 15]
+    s_t = np.float32(1.0) / np.float32(6.0)
+    assert np.float32(6.0) * s_t == np.float32(1.0)
+    c, b = oracle.quantize_nvfp4_static_f32(y.reshape(1, 16), s_t)
+    assert b.tolist() == [[0x4C]]
+    assert c.reshape(-1).tolist() == [want[2 * i] | (want[2 * i + 1] << 4) for i in range(8)]
+
+
+def test_nvfp4_static_f32_saturates_and_refuses():
+    # beyond the calibrated range: block scale 448, codes +-6
+    y = np.full((1, 16), 1e6, dtype=np.float32)
+    y[0, 1::2] = -1e6
+    c, b = oracle.quantize_nvfp4_static_f32(y, np.float32(2.0 ** -10))
+    assert b.tolist() == [[0x7E]] and c.reshape(-1).tolist() == [0xF7] * 8
+    with pytest.raises(oracle.NonFiniteInput):
+        oracle.quantize_nvfp4_static_f32(np.array([[np.inf] + [0.0] * 15], np.float32), np.float32(1.0))
+    with pytest.raises(ValueError):
+        oracle.quantize_nvfp4_static_f32(np.zeros((1, 16), np.float32), np.float32(2.0 ** -100))

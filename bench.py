@@ -44,11 +44,15 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-mib", type=int, default=600,
                     help="size of the weight pool for the cold-HBM W4A16 measurement")
-    ap.add_argument("--traffic-probe", action="store_true",
-                    help="only launch the dominant GEMM (3x per DiT shape) and a calibration copy; "
-                         "for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--traffic-probe", nargs="?", const="nvfp4", choices=("nvfp4", "fp8"),
+                    help="only launch the DiT GEMMs of one format (3x per shape) and a calibration copy; "
+                         "for rocprofv3 --pmc runs")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT_MD"),
                     help="turn the two counter runs of --traffic-probe into the traffic summary")
+    ap.add_argument("--mfma-summary", nargs=2, metavar=("PMC_DIR", "OUT_MD"),
+                    help="turn a MfmaUtil counter run of --traffic-probe into the MFMA-utilisation summary")
+    ap.add_argument("--kind", choices=("nvfp4", "fp8"), default="nvfp4",
+                    help="format of the --traffic-summary / --mfma-summary counter runs")
     ap.add_argument("--w4a16-pool-only", action="store_true",
                     help="only the cold-HBM W4A16 pool measurement (one JSON line); for rocprofv3 runs")
     return ap.parse_args()
@@ -57,7 +61,9 @@ def parse():
 # HBM traffic of the dominant kernel, measured with rocprofv3 counters (see
 # --traffic-probe / --traffic-summary) and kept as a text summary; reported
 # only while the kernel source is the one the counters were taken on.
-TRAFFIC_MD = os.path.join(ROOT, "profiles", "k_gemm_nvfp4_direct_dit_traffic.md")
+TRAFFIC_MD = {"nvfp4": os.path.join(ROOT, "profiles", "k_gemm_nvfp4_direct_dit_traffic.md"),
+              "fp8": os.path.join(ROOT, "profiles", "k_gemm_fp8_direct_dit_traffic.md")}
+KERNEL = {"nvfp4": "k_gemm_nvfp4_direct", "fp8": "k_gemm_fp8_direct"}
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_21849_amd", "csrc", "gemm.hip")
 COPY_BYTES = 512 * 2 ** 20
 
@@ -68,33 +74,36 @@ def source_sha() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def nvfp4_gemm_bytes(m, n, k):
-    """Algorithmic bytes of one W4A4 GEMM: A codes + scales, packed W codes +
-    scales, bf16 Y."""
-    return m * k * (0.5 + 1 / 16) + n * k * (0.5 + 1 / 16) + 2 * m * n
+def gemm_bytes(kind, m, n, k):
+    """Algorithmic bytes of one DiT GEMM: A codes (+ NVFP4 block scales),
+    packed W codes (+ scales), bf16 Y."""
+    per = (0.5 + 1 / 16) if kind == "nvfp4" else 1.0
+    return m * k * per + n * k * per + 2 * m * n
 
 
-def traffic_probe():
+def traffic_probe(kind):
     import torch
     import paper_2609_21849_amd as q
     import synth
     torch.cuda.set_device(0)
     M = synth.DIT_TOKENS
+    fmt = q.QG_FMT_NVFP4 if kind == "nvfp4" else q.QG_FMT_FP8_E4M3
     runs = []
     for li, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
         base = 16 * li
+        # NVFP4: the heavy-tailed activations of the step; FP8: N(0, 1)
         x = synth.normal_bf16(M, k, synth.SIGMA_X, 0, base + synth.STREAM_X,
-                              outlier_frac=synth.HEAVY_TAIL_FRAC, outlier_gain=synth.HEAVY_TAIL_GAIN,
-                              outlier_stream=base + synth.STREAM_OUTLIER)
+                              outlier_frac=synth.HEAVY_TAIL_FRAC if kind == "nvfp4" else 0.0,
+                              outlier_gain=synth.HEAVY_TAIL_GAIN, outlier_stream=base + synth.STREAM_OUTLIER)
         w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
-        a = q.quantize(dev_bf16(x), q.QG_FMT_NVFP4)
-        p = q.pack(q.quantize(dev_bf16(w), q.QG_FMT_NVFP4))
+        a = q.quantize(dev_bf16(x), fmt)
+        p = q.pack(q.quantize(dev_bf16(w), fmt))
         y = torch.empty((M, n), dtype=torch.bfloat16, device="cuda")
         runs.append((a, p, y, n))
     torch.cuda.synchronize()
     for a, p, y, n in runs:
         for _ in range(3):
-            q.linear(a, p, q.QG_FMT_NVFP4, n, y=y)
+            q.linear(a, p, fmt, n, y=y)
     torch.cuda.synchronize()
     src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
@@ -105,23 +114,64 @@ def traffic_probe():
     print("traffic probe done", flush=True)
 
 
-def traffic_summary(fetch_dir, write_dir, out_md):
+def read_counter(d, counter, kernel):
+    """Per-dispatch values of a counter for `kernel` and for the calibration
+    copy, from rocprofv3 --output-format csv runs under directory d."""
     import csv
     import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows += [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r.get("Dispatch_Id", 0)))
+    gemm = [float(r["Counter_Value"]) for r in rows if kernel in r["Kernel_Name"]]
+    copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
+            or "copy_kernel" in r["Kernel_Name"]]
+    return gemm, copy
+
+
+def mfma_summary(pmc_dir, out_md, kind):
+    """MfmaUtil, executed MFMA work and GRBM_GUI_ACTIVE of the DiT GEMMs of
+    one format, from one `rocprofv3 --pmc MfmaUtil <flops> GRBM_GUI_ACTIVE`
+    run over --traffic-probe."""
+    import synth
+    kern = KERNEL[kind]
+    flops_ctr = "MfmaFlopsF16" if kind == "nvfp4" else "SQ_INSTS_VALU_MFMA_MOPS_F8"
+    util, _ = read_counter(pmc_dir, "MfmaUtil", kern)
+    fl, _ = read_counter(pmc_dir, flops_ctr, kern)
+    gui, _ = read_counter(pmc_dir, "GRBM_GUI_ACTIVE", kern)
+    if kind == "fp8":
+        fl = [v * 512 for v in fl]
+    assert len(util) == len(fl) == len(gui) == 12, (len(util), len(fl), len(gui))
+    M = synth.DIT_TOKENS
+    lines = ["# MFMA utilisation of `%s` at the transformer shapes (M = %d)" % (kern, M), "",
+             "rocprofv3 counters over `bench.py --traffic-probe %s` (each of the four DiT-shaped %s GEMMs launched "
+             "three times): `MfmaUtil` (SQ_VALU_MFMA_BUSY_CYCLES over the SIMDs / (GRBM_GUI_ACTIVE x SIMD count) x "
+             "100), executed MFMA flops (%s%s) and GRBM_GUI_ACTIVE (summed over the 8 XCDs)."
+             % (kind, kind.upper(), flops_ctr, " x 512" if kind == "fp8" else ""), "",
+             "Command (repo root, MI355X):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc MfmaUtil %s "
+             "GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_mfma_%s -o run -- python3 bench.py "
+             "--traffic-probe %s" % (flops_ctr, kind, kind),
+             "python3 bench.py --mfma-summary gpurun_out/pmc_mfma_%s <this file> --kind %s" % (kind, kind), "```", "",
+             "| linear (M x N x K) | launch | MfmaUtil % | MFMA flops / 2MNK | GUI-active cycles / 8 |",
+             "|---|---:|---:|---:|---:|"]
+    for i, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
+        for j in range(3):
+            t = 3 * i + j
+            lines.append("| %s (%dx%dx%d) | %d | %.1f | %.4f | %.0f |" % (name, M, n, k, j + 1, util[t],
+                                                                        fl[t] / (2.0 * M * n * k), gui[t] / 8))
+    lines += ["", "Source: paper_2609_21849_amd/csrc/gemm.hip, SHA-256 prefix %s." % source_sha(), ""]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def traffic_summary(fetch_dir, write_dir, out_md, kind="nvfp4"):
     import synth
 
-    def read(d, counter):
-        rows = []
-        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            rows += [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == counter]
-        rows.sort(key=lambda r: int(r.get("Dispatch_Id", 0)))
-        gemm = [float(r["Counter_Value"]) for r in rows if "k_gemm_nvfp4_direct" in r["Kernel_Name"]]
-        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
-                or "copy_kernel" in r["Kernel_Name"]]
-        return gemm, copy
-
-    fg, fc = read(fetch_dir, "FETCH_SIZE")
-    wg, wc = read(write_dir, "WRITE_SIZE")
+    kern = KERNEL[kind]
+    fg, fc = read_counter(fetch_dir, "FETCH_SIZE", kern)
+    wg, wc = read_counter(write_dir, "WRITE_SIZE", kern)
     assert len(fg) == len(wg) == 12 and fc and wc, (len(fg), len(wg), len(fc), len(wc))
     f_factor = (sum(fc) / len(fc)) * 1024 / COPY_BYTES   # counter KiB per true byte, x1024
     w_factor = (sum(wc) / len(wc)) * 1024 / COPY_BYTES
@@ -132,21 +182,24 @@ def traffic_summary(fetch_dir, write_dir, out_md):
         fb = sum(fg[3 * i:3 * i + 3]) / 3 * 1024 / f_factor
         wb = sum(wg[3 * i:3 * i + 3]) / 3 * 1024 / w_factor
         per.append({"linear": name, "m": M, "n": n, "k": k, "fetch_bytes": round(fb), "write_bytes": round(wb),
-                    "algorithmic_bytes": round(nvfp4_gemm_bytes(M, n, k))})
+                    "algorithmic_bytes": round(gemm_bytes(kind, M, n, k))})
     t = sum(p["fetch_bytes"] + p["write_bytes"] for p in per) / len(per)
     alg = sum(p["algorithmic_bytes"] for p in per) / len(per)
-    data = {"kernel": "k_gemm_nvfp4_direct", "source": "paper_2609_21849_amd/csrc/gemm.hip",
+    data = {"kernel": kern, "source": "paper_2609_21849_amd/csrc/gemm.hip",
             "source_sha": source_sha(), "traffic_bytes_per_launch": round(t),
             "algorithmic_bytes_per_launch": round(alg), "ratio": round(t / alg, 3),
             "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib": sum(fc) / len(fc), "write_kib": sum(wc) / len(wc),
                                  "fetch_factor": round(f_factor, 4), "write_factor": round(w_factor, 4)},
             "per_shape": per}
-    lines = ["# HBM traffic of k_gemm_nvfp4_direct at the DiT shapes (M = 4608)", "",
+    lines = ["# HBM traffic of %s at the DiT shapes (M = %d)" % (kern, M), "",
              "Commands (from the repository root on the MI355X box):", "",
              "```",
-             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py --traffic-probe",
-             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py --traffic-probe",
-             "python3 bench.py --traffic-summary gpurun_out/pmc_fetch gpurun_out/pmc_write <this file>",
+             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_%s -o run -- python3 bench.py "
+             "--traffic-probe %s" % (kind, kind),
+             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_%s -o run -- python3 bench.py "
+             "--traffic-probe %s" % (kind, kind),
+             "python3 bench.py --traffic-summary gpurun_out/pmc_fetch_%s gpurun_out/pmc_write_%s <this file> --kind %s"
+             % (kind, kind, kind),
              "```", "",
              "Each counter is scaled by what it reads for a %d MiB device-to-device copy (%d MiB read, %d MiB "
              "written): fetch factor %.4f, write factor %.4f (counter KiB x 1024 / true bytes)."
@@ -162,11 +215,12 @@ def traffic_summary(fetch_dir, write_dir, out_md):
     print(json.dumps(data))
 
 
-def recorded_traffic():
-    """(bytes per launch, summary) of the committed traffic summary, or
-    (None, reason) when it is missing or was taken on another kernel source."""
+def recorded_traffic(kind):
+    """(bytes per launch, summary) of the committed traffic summary of the
+    `kind` DiT GEMM, or (None, reason) when it is missing or was taken on
+    another kernel source."""
     try:
-        txt = open(TRAFFIC_MD).read()
+        txt = open(TRAFFIC_MD[kind]).read()
         blob = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
     except (OSError, IndexError, ValueError):
         return None, "no traffic summary"
@@ -183,10 +237,13 @@ def dev_bf16(bits):
 def main():
     args = parse()
     if args.traffic_summary:
-        traffic_summary(*args.traffic_summary)
+        traffic_summary(*args.traffic_summary, kind=args.kind)
+        return
+    if args.mfma_summary:
+        mfma_summary(*args.mfma_summary, kind=args.kind)
         return
     if args.traffic_probe:
-        traffic_probe()
+        traffic_probe(args.traffic_probe)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path "
@@ -374,7 +431,7 @@ def main():
     dur_ms = sum(d for _, d in launches)
     achieved = fl / (dur_ms * 1e9)  # TFLOP/s
     peak = PEAK["fp8"] if dom == "fp8" else PEAK["f16"]
-    traffic, tinfo = recorded_traffic() if dom == "nvfp4" else (None, "counters taken for the W4A4 kernel only")
+    traffic, tinfo = recorded_traffic(dom)
     roofline = {"bound": "mfma",
                 "kernel": "k_gemm_fp8_direct (W8A8, fp8 MFMA)" if dom == "fp8" else "k_gemm_nvfp4_direct (W4A4, fp16 MFMA)",
                 "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",

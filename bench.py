@@ -303,7 +303,8 @@ def main():
     t_setup = time.time() - t_setup
 
     # ------------------------------------------------------------ the step as a flat launch list
-    # (integer pointers and a fixed stream handle keep per-launch host overhead small)
+    # (integer pointers keep per-launch host overhead small; the stream handle
+    # is appended at launch time, so that the list can also be captured)
     lib = q.lib()
     st = torch.cuda.current_stream().cuda_stream
     plan = []
@@ -313,26 +314,26 @@ def main():
             bs = a.block_scales.data_ptr() if a.block_scales is not None else None
             plan.append((("quant", kind, e["name"]), lib.qg_quantize_act,
                          (fmt, x.data_ptr(), M, e["k"], e["k"], a.codes.data_ptr(), bs,
-                          a.tensor_scale.data_ptr(), st)))
+                          a.tensor_scale.data_ptr())))
             plan.append((("gemm", kind, e["name"]), lib.qg_gemm,
                          (fmt, a.codes.data_ptr(), bs, a.tensor_scale.data_ptr(), e["k"], fmt,
                           wp.data_ptr(), wp.numel(), M, e["n"], e["k"], y.data_ptr(), e["n"],
-                          q.QG_OUT_BF16, st)))
+                          q.QG_OUT_BF16)))
     for e in enc:
         plan.append((("gemm", "w4a16", "%s_m%d" % (e["name"], e["m"])), lib.qg_gemm,
                      (q.QG_FMT_BF16, e["x"].data_ptr(), None, None, e["k"], q.QG_FMT_NVFP4,
                       e["w"].data_ptr(), e["w"].numel(), e["m"], e["n"], e["k"], e["y"].data_ptr(),
-                      e["n"], q.QG_OUT_BF16, st)))
+                      e["n"], q.QG_OUT_BF16)))
 
     def make_events(n):
         return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
 
-    def step(events):
-        """One pass of the launch list; events[i] (or None) brackets launch i."""
+    def step(events, stream=st):
+        """One pass of the launch list on `stream`; events[i] (or None) brackets launch i."""
         for (key, fn, fargs), ev in zip(plan, events):
             if ev is not None:
                 ev[0].record()
-            rc = fn(*fargs)
+            rc = fn(*fargs, stream)
             if ev is not None:
                 ev[1].record()
             if rc != 0:
@@ -357,6 +358,11 @@ def main():
     dom = max(shares, key=shares.get)
     dom_idx = [i for i, (key, _, _) in enumerate(plan) if key[0] == "gemm" and key[1] == dom]
 
+    # The timed steps: the launch list run --steps times, with events around
+    # the launches of the dominant kernel (their durations give the roofline).
+    # (ROCm's torch does not allow event-record nodes in captured graphs, so
+    # the timed region is the eager launch loop; the graph-replayed step time
+    # is reported beside it in parts.)
     step_events = []
     for _ in range(args.steps):
         ev = [None] * len(plan)
@@ -378,6 +384,10 @@ def main():
     for evs in step_events:
         for i in dom_idx:
             dom_live.setdefault(plan[i][0], []).append(evs[i][0].elapsed_time(evs[i][1]))
+    timing_mode = "eager launches (events around the dominant kernel)"
+    # the same step as a graph replay without any inner event (GPU time of the
+    # launch list with no host launch latency between launches), for context
+    graph_step_us = graph_us(lambda s: step([None] * len(plan), s), reps=args.steps)
 
     # ------------------------------------------------------------ accounting
     def flops(e, m=M):
@@ -411,10 +421,17 @@ def main():
         ms = float(np.mean(durations.get(("gemm", "w4a16", key))))
         byt = e["n"] * e["k"] * 0.5625 + e["m"] * e["k"] * 2 + e["m"] * e["n"] * 2
         total_flops += flops(e, e["m"])
+        args_w = next(fa for (k2, _, fa) in plan if k2 == ("gemm", "w4a16", key))
+        gus = graph_us(lambda s: lib.qg_gemm(*args_w, s))
         w4[key] = {"us": round(ms * 1e3, 2), "gbs": round(byt / (ms * 1e6), 1),
-                   "tflops": round(flops(e, e["m"]) / (ms * 1e9), 2)}
+                   "tflops": round(flops(e, e["m"]) / (ms * 1e9), 2),
+                   "graph_us": round(gus, 2) if gus else None,
+                   "graph_gbs": round(byt / (gus * 1e3), 1) if gus else None}
     parts["w4a16_single_call"] = w4
+    parts["w4a16_single_call_note"] = ("us: HIP events around the call in the instrumented step (host launch "
+                                       "latency included); graph_us: GPU time per call from graph replays")
     parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
+    parts["graph_replay_ms_per_step"] = round(graph_step_us / 1e3, 4) if graph_step_us else None
     parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
     parts["mx"] = mx_part(q, lib, st, dit, M, flops, parts["nvfp4"], parts["fp8"])
     parts["dit_block_chain"] = block_chain_part(q, dit, M)
@@ -474,6 +491,7 @@ def main():
         "roofline": roofline,
         "headline": headline,
         "parts": parts,
+        "timing": timing_mode,
         "setup_s": round(t_setup, 1),
         "timed_wall_s": round(wall, 3),
     }
@@ -482,12 +500,42 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def graph_us(fn, reps=40):
+    """GPU time per call of fn(stream) (microseconds): `reps` calls captured in
+    a HIP graph, the replay timed with events (no host launch latency between
+    the calls); None where the runtime cannot capture them."""
+    import torch
+    try:
+        cs = torch.cuda.Stream()
+        with torch.cuda.stream(cs):
+            fn(cs.cuda_stream)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            for _ in range(reps):
+                fn(cs.cuda_stream)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (3 * reps) * 1e3
+    except Exception as ex:
+        print("graph timing unavailable (%s)" % str(ex)[:200], file=sys.stderr)
+        return None
+
+
 def single_linear_part(q, synth, reps=50):
     """The two single-linear configurations: FP8 W8A8 128x256x256 and NVFP4
     W4A4 512x3072x3072 (X ~ N(0,1), W ~ N(0,0.02), seed 0), each call the
     dynamic activation quantize plus the GEMM through the C ABI (the weight
-    quantized and packed offline). HIP events around each launch; medians
-    over `reps` calls. The NVFP4 GEMM is placed against its roofline:
+    quantized and packed offline). GPU time per call from graph replays;
+    beside it the median of `reps` calls bracketed by HIP events one by one
+    (which includes the host's launch latency). The NVFP4 GEMM is placed
+    against its roofline:
     max(2MNK / peak, algorithmic bytes / HBM peak) for the fp16 matrix rate
     it runs on, and for the fp4 peak the format nominally targets."""
     import torch
@@ -516,13 +564,18 @@ def single_linear_part(q, synth, reps=50):
             assert lib.qg_gemm(*gargs) == 0
             evs[i][2].record()
         torch.cuda.synchronize()
-        qus = float(np.median([ev[0].elapsed_time(ev[1]) for ev in evs[5:]])) * 1e3
-        gus = float(np.median([ev[1].elapsed_time(ev[2]) for ev in evs[5:]])) * 1e3
+        qus_l = float(np.median([ev[0].elapsed_time(ev[1]) for ev in evs[5:]])) * 1e3
+        gus_l = float(np.median([ev[1].elapsed_time(ev[2]) for ev in evs[5:]])) * 1e3
+        # GPU time per call from graph replays (the host's launch latency, a
+        # few microseconds per call, is part of the event-pair figures above)
+        qus = graph_us(lambda s: lib.qg_quantize_act(*qargs[:-1], s)) or qus_l
+        gus = graph_us(lambda s: lib.qg_gemm(*gargs[:-1], s)) or gus_l
         flops = 2.0 * m * n * k
         wbytes = n * k * (0.5625 if nv else 1.0)
         abytes = m * k * (0.5625 if nv else 1.0)
         gbytes = wbytes + abytes + m * n * 2
         ent = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2), "linear_us": round(qus + gus, 2),
+               "with_host_launch": {"quant_us": round(qus_l, 2), "gemm_us": round(gus_l, 2)},
                "gemm_tflops": round(flops / (gus * 1e6), 1), "gemm_algorithmic_mb": round(gbytes / 1e6, 2)}
         if nv:
             t_f16 = max(flops / (PEAK["f16"] * 1e12), gbytes / (PEAK["hbm_gbs"] * 1e9)) * 1e6
@@ -539,7 +592,8 @@ def single_linear_part(q, synth, reps=50):
 def w8a8_encoder_part(q, enc, reps=20):
     """W8A8 at the text-encoder shapes (the FP8 alternative to W4A16 for the
     small encoder): dynamic activation quantize + FP8 GEMM per call, with
-    preallocated buffers and raw C-ABI launches (HIP events per launch)."""
+    preallocated buffers and raw C-ABI launches: GPU time per call from graph
+    replays, and the HIP-event time per launch (host launch latency included)."""
     import torch
     lib = q.lib()
     st = torch.cuda.current_stream().cuda_stream
@@ -560,10 +614,13 @@ def w8a8_encoder_part(q, enc, reps=20):
             assert lib.qg_gemm(*gargs) == 0
             evs[i][2].record()
         torch.cuda.synchronize()
-        qus = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in evs[3:]])) * 1e3
-        gus = float(np.mean([ev[1].elapsed_time(ev[2]) for ev in evs[3:]])) * 1e3
+        qus_l = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in evs[3:]])) * 1e3
+        gus_l = float(np.mean([ev[1].elapsed_time(ev[2]) for ev in evs[3:]])) * 1e3
+        qus = graph_us(lambda s: lib.qg_quantize_act(*qargs[:-1], s)) or qus_l
+        gus = graph_us(lambda s: lib.qg_gemm(*gargs[:-1], s)) or gus_l
         out["%s_m%d" % (e["name"], m)] = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2),
-                                            "gemm_tflops": round(2 * m * n * k / (gus * 1e6), 2)}
+                                            "gemm_tflops": round(2 * m * n * k / (gus * 1e6), 2),
+                                            "with_host_launch": {"quant_us": round(qus_l, 2), "gemm_us": round(gus_l, 2)}}
     return out
 
 

@@ -157,6 +157,9 @@ qg_status qg_quantize_act_static(qg_format fmt, const void *x, int64_t rows, int
  * qg_packed_bytes -- size of the packed weight buffer for an [n, k] weight
  * in `fmt` (FP8, NVFP4, MXFP4 or MXFP8), or 0 when the shape breaks the GEMM
  * contract (n % 16, k % 128; MX k % 256) or the format is not packable.
+ * Paper: Sec. 4, quantization and weight-streaming paragraphs (the bytes a
+ * quantized layer occupies are the W of the streaming cost model below).
+ * Host-only; touches no device memory.
  */
 size_t qg_packed_bytes(qg_format fmt, int64_t n, int64_t k);
 
@@ -180,8 +183,15 @@ qg_status qg_pack_weights(qg_format fmt, const void *codes, const void *block_sc
 
 /*
  * qg_unpack_weights -- inverse of qg_pack_weights: writes the canonical
- * codes, block scales (NVFP4) and tensor scale back out. For tests and for
- * tools that need the weights in the canonical layout.
+ * codes, block scales (NVFP4, MX) and tensor scale (FP8, NVFP4) back out.
+ * Paper: Sec. 4, quantization paragraph (the PTQ weight as quantized: the
+ * formats above). For tests and for tools that need the weights in the
+ * canonical layout. Arguments are checked as in qg_pack_weights
+ * (packed_bytes < qg_packed_bytes(fmt, n, k): QG_ERR_BUFFER_TOO_SMALL). The
+ * header sits in device memory and is not read on the host: fmt, n and k
+ * must be those of the qg_pack_weights call, else the outputs are
+ * unspecified. Outputs are dense like qg_quantize_act's (block_scales NULL
+ * for FP8; tensor_scale NULL for MX).
  */
 qg_status qg_unpack_weights(qg_format fmt, const void *packed, size_t packed_bytes,
                             int64_t n, int64_t k, void *codes, void *block_scales,
@@ -284,6 +294,8 @@ qg_status qg_gemm_quant_nvfp4(qg_format a_fmt, const void *a, const void *a_bloc
 
 /*
  * qg_dequant -- decode a quantized tensor to bf16 or fp32.
+ * Paper: Sec. 4, quantization paragraph (the value a code stands for in each
+ * cited format: the decode side of the quantizers above).
  *   FP8  : out = fl(e4m3(q) * s)
  *   NVFP4: out = fl(fl(e2m1(q) * e4m3(s_b)) * s_t)   (the inner product is exact)
  *   MX   : out = e2m1 / e4m3(q) * 2^(e-127)                  (exact in fp32)

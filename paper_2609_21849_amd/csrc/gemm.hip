@@ -1216,8 +1216,10 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
       load_a(kc);
       write_a(smem);
       __syncthreads();
-      load_a(kc + 1);
+      // weights of chunk kc before activations of kc + 1: the order the loop
+      // issues them in, so that the loop head's waits count the same loads
       load_b(std::integral_constant<int, 0>(), kc);
+      load_a(kc + 1);
       fa[0] = read_a_frag(smem, wm * 4, 0, lane);
       for (; kc < kcn; kc += 2) {
         chunk(std::integral_constant<int, 0>(), kc);
@@ -1231,6 +1233,255 @@ __global__ void __launch_bounds__(256) k_gemm_fp8_direct(GemmArgs g) {
       store_tiles_fast<4, 4>(g, acc, sout + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, scale);
     else
       store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, scale);
+  }
+}
+
+// ---------------------------------------------------------------- FP8, 288 x 192 tiles
+// At the transformer shapes (M = 4608, N = 3072 or 9216) 256 x 256 tiles
+// number 216 or 648 on 256 CUs, so one round of tiles in every three (or the
+// only round) runs 16-47% empty, and the kernel's time follows the number of
+// rounds (measured: 1.0, 2.0 and 3.0 rounds' time at 0.84, 1.97 and 2.53
+// rounds of tiles). 288 x 192 tiles give exactly 256 or 768 tiles there.
+// Four waves in 2 x 2, each 144 x 96 = 9 x 6 blocks of
+// v_mfma_f32_16x16x128_f8f6f4, which runs at the 32x32x64 instruction's rate
+// (4.69 PFLOP/s with 54 independent accumulators, one wave per SIMD), so the
+// tile needs no 32-row granularity in M.
+//   weights     : fragment (16 rows x 128 K) of lane l = row l % 16, bytes
+//                 32 (l / 16) .. + 31 of the row's chunk; in the packed FP8
+//                 image those are pieces h = 0, 1 of step t = l / 32, lane
+//                 half g = (l / 16) % 2, so each 16-byte wave load reads four
+//                 contiguous 256-byte runs. Loaded straight into registers one
+//                 chunk ahead, two register sets.
+//   activations : staged in LDS per chunk as 18 blocks of 16 rows x 128 B;
+//                 piece c (16 B) of row i of a block sits in slot
+//                 8 i + (c ^ f(i)), f(i) = (i & 7) ^ (i >> 3): the eight
+//                 lanes that stage one row, and the fragment reads (lane l:
+//                 row l % 16, pieces 2 (l / 16) and 2 (l / 16) + 1), hit
+//                 distinct bank groups for 32 and for 64 banks (checked on the
+//                 CPU).
+// Output: lane l of block (i, j) holds Y[m0 + 16 i + l % 16][n0 + 16 j +
+// 4 (l / 16) + e], four consecutive outputs of a row. bf16, fp32 and FP8
+// outputs; the NVFP4 output keeps the 256 x 256 kernel.
+struct AStage288 {
+  static constexpr int RA = 9;  // 16-byte pieces per thread per chunk
+  uint32_t oa[RA], la[RA];
+  __device__ __attribute__((always_inline)) inline void init(const GemmArgs& g, int m0, int tid) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) {
+      const int q = it * 256 + tid;
+      const int row = q >> 3, c = q & 7, i = row & 15;
+      const uint32_t grow = (uint32_t)(m0 + row);
+      oa[it] = (grow < (uint32_t)g.m) ? grow * (uint32_t)g.lda + 16u * c : 0x80000000u;
+      la[it] = (uint32_t)((row >> 4) * 2048 + i * 128 + ((c ^ ((i & 7) ^ (i >> 3))) * 16));
+    }
+  }
+};
+
+__device__ __attribute__((always_inline)) inline v8i read_a16(const uint8_t* st, int blk, int lane) {
+  const int i = lane & 15, q = lane >> 4, f = (i & 7) ^ (i >> 3);
+  const uint8_t* p = st + blk * 2048 + i * 128;
+  const v4i lo = *reinterpret_cast<const v4i*>(p + (((2 * q) ^ f) * 16));
+  const v4i hi = *reinterpret_cast<const v4i*>(p + (((2 * q + 1) ^ f) * 16));
+  return (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+}
+
+__global__ void __launch_bounds__(256) k_gemm_fp8_t288(GemmArgs g) {
+  constexpr int A_STAGE = 18 * 2048;
+  constexpr int RA = AStage288::RA;
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int OPITCH = 96 * 2 + 16;           // output staging: 16 rows of 96 bf16 + pad
+  constexpr int OUT_STAGE = 16 * OPITCH;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t sout[4 * OUT_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const float scale = *g.w_tscale * *g.a_tscale;
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const __amdgpu_buffer_rsrc_t rs_a = rsrc_a_fp8(g);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 4096), 0x00020000);
+  // lane part of a weight fragment's offset inside a panel's chunk
+  const uint32_t lane_b = (uint32_t)((lane >> 5) * 2048 + ((lane & 15) + 32 * ((lane >> 4) & 1)) * 16);
+
+  AStage288 A;
+  uint32_t ob[3];
+  v4i ga[RA];
+  v8i fb[2][6];  // [chunk parity][16-row weight fragment]
+  v8i fa[2];
+  v4f acc[9][6];
+
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
+  auto load_a = [&](int kc) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it)
+      ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], kcl(kc) * 128, 0);
+  };
+  auto write_a = [&](uint8_t* st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < RA; ++it) *reinterpret_cast<v4i*>(st + A.la[it]) = ga[it];
+  };
+  auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const int so = kcl(kc) * 4096;
+#pragma unroll
+    for (int jj = 0; jj < 6; ++jj) {
+      const uint32_t o = ob[jj >> 1] + (jj & 1) * 256;
+      const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o, so, 0);
+      const v4i hi = __builtin_amdgcn_raw_buffer_load_b128(rs_b, o + 1024, so, 0);
+      fb[P][jj] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    }
+  };
+  // MFMA group f: activation block f of the wave against its six weight fragments
+  auto mgroup = [&](auto Pc, int f, int slot) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int jj = 0; jj < 6; ++jj)
+      acc[f][jj] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fb[P][jj], fa[slot], acc[f][jj], 0, 0, 0, 0, 0, 0);
+  };
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    // groups 0, 1: weight loads of chunk kc + 1 (12 per lane)
+    load_b(std::integral_constant<int, P ^ 1>(), kc + 1);
+#pragma unroll
+    for (int f = 0; f < 3; ++f) {
+      fa[(f + 1 + P) & 1] = read_a16(cur, wm * 9 + f + 1, lane);
+      mgroup(Pc, f, (f + P) & 1);
+    }
+#pragma unroll
+    for (int f = 0; f < 3; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 6; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (f < 2) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (weights)
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // groups 3..7: stage the activations of chunk kc + 1 (two pieces per
+    // group, the last group one), then load chunk kc + 2 into the same registers
+    const int a_so = kcl(kc + 2) * 128;
+#pragma unroll
+    for (int f = 3; f < 8; ++f) {
+      fa[(f + 1 + P) & 1] = read_a16(cur, wm * 9 + f + 1, lane);
+#pragma unroll
+      for (int it = 2 * (f - 3); it < 2 * (f - 2) && it < RA; ++it)
+        *reinterpret_cast<v4i*>(nxt + A.la[it]) = ga[it];
+      mgroup(Pc, f, (f + P) & 1);
+#pragma unroll
+      for (int it = 2 * (f - 3); it < 2 * (f - 2) && it < RA; ++it)
+        ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, A.oa[it], a_so, 0);
+    }
+#pragma unroll
+    for (int f = 3; f < 8; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read: next fragment
+#pragma unroll
+      for (int t = 0; t < 6; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (t < 2 && 2 * (f - 3) + t < RA) {
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (activations)
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // group 8 covers the read of the next chunk's first fragment
+    fa[(9 + P) & 1] = read_a16(nxt, wm * 9, lane);
+    mgroup(Pc, 8, (8 + P) & 1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 288, n0 = bn * 192;
+    A.init(g, m0, tid);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 3 + j);
+      ob[j] = (panel < (uint32_t)npanels_w) ? panel * (uint32_t)(kcn * 4096) + lane_b : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int j = 0; j < 6; ++j) acc[i][j] = (v4f){0.0f, 0.0f, 0.0f, 0.0f};
+
+    // An odd chunk count takes its first chunk unpipelined, so that the
+    // pipelined loop runs whole pairs of chunks (register set 0, then 1).
+    int kc = 0;
+    if (kcn & 1) {
+      load_a(0);
+      write_a(smem);
+      load_b(std::integral_constant<int, 0>(), 0);
+      __syncthreads();
+#pragma unroll
+      for (int f = 0; f < 9; ++f) {
+        fa[f & 1] = read_a16(smem, wm * 9 + f, lane);
+        mgroup(std::integral_constant<int, 0>(), f, f & 1);
+      }
+      __syncthreads();
+      kc = 1;
+    }
+    if (kc < kcn) {
+      load_a(kc);
+      write_a(smem);
+      __syncthreads();
+      // weights of chunk kc before activations of kc + 1: the order the loop
+      // issues them in, so that the loop head's waits count the same loads
+      load_b(std::integral_constant<int, 0>(), kc);
+      load_a(kc + 1);
+      fa[0] = read_a16(smem, wm * 9, lane);
+      for (; kc < kcn; kc += 2) {
+        chunk(std::integral_constant<int, 0>(), kc);
+        chunk(std::integral_constant<int, 1>(), kc + 1);
+      }
+    }
+    const int mw = m0 + wm * 144, nw = n0 + wn * 96;
+    if (fast_out && m0 + 288 <= g.m && n0 + 192 <= g.n) {
+      // each 16-row block of the wave through its private LDS area, read back
+      // in row order so that every store writes whole 192-byte row segments
+      uint8_t* st = sout + wave * OUT_STAGE;
+      uint8_t* wr = st + (lane & 15) * OPITCH + 8 * (lane >> 4);
+#pragma unroll
+      for (int i = 0; i < 9; ++i) {
+#pragma unroll
+        for (int jj = 0; jj < 6; ++jj)
+          *reinterpret_cast<uint2*>(wr + 32 * jj) =
+              make_uint2(pk_bf16(acc[i][jj][0] * scale, acc[i][jj][1] * scale),
+                         pk_bf16(acc[i][jj][2] * scale, acc[i][jj][3] * scale));
+#pragma unroll
+        for (int it = 0; it < 3; ++it) {
+          const int idx = it * 64 + lane, row = idx / 12, pc = idx - 12 * (idx / 12);
+          const uint4 v = *reinterpret_cast<const uint4*>(st + row * OPITCH + pc * 16);
+          *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(g.y) +
+                                    ((int64_t)(mw + 16 * i + row) * g.ldy + nw + 8 * pc) * 2) = v;
+        }
+      }
+    } else {
+      const bool vec = out_vec(g);
+      const float ry = out_rscale(g);
+#pragma unroll
+      for (int i = 0; i < 9; ++i) {
+        const int m = mw + 16 * i + (lane & 15);
+        if (m >= g.m) continue;
+#pragma unroll
+        for (int jj = 0; jj < 6; ++jj) {
+          const int n = nw + 16 * jj + 4 * (lane >> 4);
+          if (n >= g.n) continue;
+          store4(g, m, n, acc[i][jj][0] * scale, acc[i][jj][1] * scale, acc[i][jj][2] * scale,
+                 acc[i][jj][3] * scale, vec, ry);
+        }
+      }
+    }
   }
 }
 
@@ -2457,6 +2708,18 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     // times as many workgroups win. Measured crossover (encoder and
     // transformer widths, M = 128 .. 3072): below 3/8 of a tile per CU.
     if (m <= 128 || 8 * tiles < 3 * cus) return run_fp8<1, 2>(g, st);
+    // 288 x 192 tiles where their rounds of tiles cover less area than the
+    // 256 x 256 tiles' rounds (the time of both kernels follows the round
+    // count); not for NVFP4 outputs, whose 16-blocks the 256 x 256 epilogue forms
+    const int t288_m = (int)((m + 287) / 288), t288_n = (int)((n + 191) / 192);
+    const int64_t t288 = (int64_t)t288_m * t288_n;
+    if (out_mode != OUT_NVFP4 &&
+        ((t288 + cus - 1) / cus) * (288 * 192) < (int64_t)((tiles + cus - 1) / cus) * (256 * 256)) {
+      g.tiles_m = t288_m;
+      g.tiles_n = t288_n;
+      hipLaunchKernelGGL(k_gemm_fp8_t288, dim3((unsigned)std::min<int64_t>(t288, cus)), dim3(256), 0, st, g);
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_gemm_fp8_direct, dim3(std::min(tiles, cus)), dim3(256), 0, st, g);
     return hipGetLastError();
   } else if (a_fmt == 2) {
@@ -2465,15 +2728,18 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     const int tiles = g.tiles_m * g.tiles_n;
     // Below half a round of 256 x 256 tiles the split-K kernel is faster
     // (measured up to M = 2300 at N = K = 3072: 0.9x the time there, 0.3x at
-    // M = 512). Tile and split: 64 x 96 tiles, four waves, where they fill
-    // the chip with K >= 2048 (the most MFMAs per expanded operand);
-    // 32 x 64 tiles, eight waves, where that leaves CUs idle; 64 x 64 tiles,
-    // four waves, for short reductions (K < 2048).
+    // M = 512). Tile and split: 64 x 96 tiles where they fill the chip with
+    // K >= 2048 (the most MFMAs per expanded operand); 32 x 64 tiles where
+    // that leaves CUs idle; 64 x 64 tiles for short reductions (K < 2048).
+    // Eight waves, two per SIMD, so that one wave's operand expansion runs
+    // beside the other's MFMAs: at 64 x 96 and 64 x 64, one chunk in flight
+    // per wave was 10-21% faster than four waves with two or three (NVFP4
+    // 512 x 3072 x 3072 16.3 -> 14.3 us, 256 x 3072 x 1024 8.1 -> 6.4 us).
     if (m <= 128 || 2 * tiles < cus) {
       const int kcn = (int)(k >> 7);
       const int64_t t6496 = (int64_t)((m + 63) / 64) * ((n + 95) / 96);
-      if (kcn < 16) return run_splitk<MODE_NVFP4, 2, 2, 4, 3>(g, st);
-      if (t6496 >= cus - cus / 4) return run_splitk<MODE_NVFP4, 2, 3, 4, 2>(g, st);
+      if (kcn < 16) return run_splitk<MODE_NVFP4, 2, 2, 8, 1>(g, st);
+      if (t6496 >= cus - cus / 4) return run_splitk<MODE_NVFP4, 2, 3, 8, 1>(g, st);
       return run_splitk<MODE_NVFP4, 1, 2, 8, 3>(g, st);
     }
     hipLaunchKernelGGL(k_gemm_nvfp4_direct, dim3(std::min(tiles, cus)), dim3(256), 0, st, g);

@@ -214,6 +214,25 @@ def test_mid_m_linear_sampled(kind, m, n, k):
     log("  max err/B", check_linear(y, ref, rows, cols))
 
 
+@pytest.mark.parametrize("m,n,k,out", [(4600, 9200, 3072, q.QG_OUT_BF16), (4608, 3072, 1152, q.QG_OUT_F32),
+                                       (4321, 3056, 640, q.QG_OUT_BF16), (4321, 3056, 640, q.QG_OUT_F32)])
+def test_fp8_whole_round_tiles_sampled(m, n, k, out):
+    # shapes the FP8 GEMM runs on 288 x 192 tiles (whole rounds of tiles):
+    # ragged rows and columns (4321 leaves one valid row in the last tile
+    # row, 3056 and 9200 a part-filled last weight panel), an odd number of
+    # 128-wide chunks (K = 1152, 640), bf16 and fp32 outputs
+    log("fp8 288x192 tiles %dx%dx%d out=%d" % (m, n, k, out))
+    x = synth.normal_bf16(m, k, 1.0, 9, 0)
+    w = synth.normal_bf16(n, k, 0.02, 9, 1)
+    y = run_linear("fp8", x, w, out, check_codes=False)
+    rows, cols = _sample(m, n, 2000, 10)
+    # the last row and the last columns of every tile edge are sampled too
+    rows = np.concatenate([rows, np.full(192, m - 1), np.resize(np.arange(0, m, 288), 192)])
+    cols = np.concatenate([cols, np.arange(n - 192, n), np.resize(np.arange(191, n, 192), 192)])
+    ref = oracle.linear_reference("fp8", x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))
+
+
 @pytest.mark.parametrize("name", list(synth.ENCODER_LINEARS))
 @pytest.mark.parametrize("m", synth.ENCODER_TOKENS)
 def test_w4a16_encoder_full(name, m):

@@ -2210,6 +2210,230 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------------- W4A16, large token counts
+// W4A16 (bf16 activations, NVFP4 weights) past the ridge point: the tile and
+// wave layout of the W4A4 kernel (256 x 256 tiles, four waves of 128 x 128,
+// persistent grid), on v_mfma_f32_32x32x16_bf16.
+//   weights     : codes and E4M3 block scales straight from the packed buffer
+//                 into registers one chunk ahead (as in k_gemm_nvfp4_direct);
+//                 each 8-code step fragment is expanded to bf16 with its block
+//                 scale (exact: E2M1 x E4M3 has at most 6 significant bits):
+//                 4 conversions to fp32, 8 multiplies, 4 byte permutes (gfx950
+//                 has no packed bf16 multiply);
+//   activations : bf16 rows staged in LDS per chunk (256 rows x 256 B). The
+//                 reduction order is the weights' permuted one: step s, lane
+//                 half g holds k = 64 g + 8 s + [0, 8), the 16-byte piece
+//                 c = 8 g + s of the row's chunk. Piece c of row r of a panel
+//                 sits in 1 KiB step block s at slot (r + 32 g) ^ (s + 8 g): the
+//                 16 lanes that stage one row and the fragment reads of any 8
+//                 or 16 neighbouring lanes fall into distinct bank groups (32
+//                 or 64 banks; checked on the CPU). Staged through registers
+//                 in two batches of eight pieces per thread per chunk.
+// One barrier per chunk, after step 6; step 7 reads the next chunk's first
+// fragments. The bf16 output staging of the epilogue reuses activation
+// stage 1, which no wave reads after the last chunk's barrier (a tile's
+// chunks run in pairs, stage 0 then 1), and the next tile writes it only
+// after its first barrier.
+__global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
+  constexpr int A_STAGE = 8 * 8192;              // 256 rows x 128 bf16
+  constexpr int OUT_STAGE = 32 * (64 * 4 + 16);
+  constexpr uint32_t OOB = 0x80000000u;
+  static_assert(4 * OUT_STAGE <= A_STAGE, "the output staging fits in one activation stage");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * A_STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 31, gq = lane >> 5;
+  const int kcn = g.k >> 7;
+  const int npanels_w = (g.n + 31) >> 5;
+  const int total = g.tiles_m * g.tiles_n;
+  const float scale = *g.w_tscale;
+  const bool fast_out = g.out_mode == OUT_BF16 && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && ((g.ldy & 7) == 0);
+  const uint32_t lda2 = (uint32_t)(g.lda * 2);
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.a), 0, (int)((int64_t)(g.m - 1) * lda2 + g.k * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * 2048), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_bs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(g.w_scales), 0, (int)((int64_t)npanels_w * kcn * 256), 0x00020000);
+  // staging: thread tid copies piece c = tid % 16 of rows 16 i + tid / 16,
+  // i = 0 .. 15; its LDS slots depend only on i % 2 (and i / 2 through the
+  // panel, a constant offset)
+  const int cpc = tid & 15, s_c = cpc & 7, g_c = cpc >> 3, rlo = tid >> 4;
+  uint32_t la_pair[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    la_pair[h] = (uint32_t)(s_c * 1024 + ((((16 * h + rlo) + 32 * g_c) ^ (s_c + 8 * g_c)) * 16));
+
+  uint32_t oa[16], ob[4], osb[4];
+  v4i ga[8];            // one staging batch
+  v4i bc[2][4][2];      // weight codes [chunk parity][panel][half]
+  uint32_t bs[2][4];    // weight E4M3 scales [chunk parity][panel]
+  float sw[4][4];       // weight block scales of the current chunk, fp32 [panel][block]
+  v8bf fa[2][4], fb[2][4];
+  v16f acc[4][4];
+
+  auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
+  auto load_a = [&](int kc, int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < 8; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[8 * b + it], kcl(kc) * 256, 0);
+  };
+  auto write_a = [&](uint8_t* st, int b, int from, int to) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int i = 8 * b + it;
+      if (it >= from && it < to) *reinterpret_cast<v4i*>(st + (i >> 1) * 8192 + la_pair[i & 1]) = ga[it];
+    }
+  };
+  auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const int kq = kcl(kc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      bc[P][j][0] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j], kq * 2048, 0);
+      bc[P][j][1] = __builtin_amdgcn_raw_buffer_load_b128(rs_b, ob[j] + 1024, kq * 2048, 0);
+      bs[P][j] = __builtin_amdgcn_raw_buffer_load_b32(rs_bs, osb[j], kq * 256, 0);
+    }
+  };
+  auto read_a = [&](const uint8_t* st, int s, int D) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      fa[D][i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4i*>(
+          st + (wm * 4 + i) * 8192 + s * 1024 + ((lane ^ (s + 8 * gq)) * 16)));
+  };
+  // the lane's four E4M3 block scales of each panel, exactly (never negative or NaN)
+  auto convert_b_scales = [&](auto Pc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)bs[P][j], false);
+      const v2f hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)bs[P][j], true);
+      sw[j][0] = lo[0]; sw[j][1] = lo[1]; sw[j][2] = hi[0]; sw[j][3] = hi[1];
+    }
+  };
+  auto expand = [&](auto Pc, int s, int D) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const v4i c = bc[P][j][s >> 2];
+      const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
+      fb[D][j] = __builtin_bit_cast(v8bf, dequant8_bf16(w, sw[j][s >> 1]));
+    }
+  };
+  auto mfmas = [&](int D) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[D][j], fa[D][i], acc[i][j], 0, 0, 0);
+  };
+  // 16 MFMAs, each followed by its share of the next step's expansion (64 VALU)
+  auto interleave = [&](int nvmem, int nds_r, int nds_w) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+      if (t < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if (t < nds_r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (t < nds_w) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    }
+  };
+
+  auto chunk = [&](auto Pc, int kc) __attribute__((always_inline)) {
+    constexpr int P = decltype(Pc)::value;
+    const uint8_t* cur = smem + P * A_STAGE;
+    uint8_t* nxt = smem + (P ^ 1) * A_STAGE;
+    constexpr std::integral_constant<int, P ^ 1> Q{};
+#pragma unroll
+    for (int s = 0; s < 7; ++s) {
+      // step 0: weights of chunk kc + 1 and the first activation batch of
+      // kc + 1; step 3: that batch into LDS, the second batch loaded; step 6:
+      // the second batch into LDS
+      if (s == 0) { load_b(Q, kc + 1); load_a(kc + 1, 0); }
+      if (s == 3) { write_a(nxt, 0, 0, 8); load_a(kc + 1, 1); }
+      if (s == 5) write_a(nxt, 1, 0, 4);
+      if (s == 6) write_a(nxt, 1, 4, 8);
+      read_a(cur, s + 1, (s + 1) & 1);
+      mfmas(s & 1);
+      expand(Pc, s + 1, (s + 1) & 1);
+      interleave(s == 0 ? 20 : s == 3 ? 8 : 0, 4, (s == 3) ? 8 : (s >= 5) ? 4 : 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    // step 7 covers the next chunk's first reads and its step-0 expansion
+    read_a(nxt, 0, 0);
+    convert_b_scales(Q);
+    mfmas(1);
+    expand(Q, 0, 0);
+    interleave(0, 4, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int bm, bn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, bm, bn);
+    const int m0 = bm * 256, n0 = bn * 256;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t row = (uint32_t)(m0 + 16 * i + rlo);
+      oa[i] = (row < (uint32_t)g.m) ? row * lda2 + 16u * cpc : OOB;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t panel = (uint32_t)((n0 >> 5) + wn * 4 + j);
+      const bool in = panel < (uint32_t)npanels_w;
+      ob[j] = in ? panel * (uint32_t)(kcn * 2048) + 16u * lane : OOB;
+      osb[j] = in ? panel * (uint32_t)(kcn * 256) + 8u * r + 4u * gq : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    // An odd chunk count takes its first chunk unpipelined.
+    int kc = 0;
+    if (kcn & 1) {
+      load_b(std::integral_constant<int, 0>(), 0);
+      load_a(0, 0);
+      write_a(smem, 0, 0, 8);
+      load_a(0, 1);
+      write_a(smem, 1, 0, 8);
+      __syncthreads();
+      convert_b_scales(std::integral_constant<int, 0>());
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        read_a(smem, s, 0);
+        expand(std::integral_constant<int, 0>(), s, 0);
+        mfmas(0);
+      }
+      __syncthreads();
+      kc = 1;
+    }
+    if (kc < kcn) {
+      load_b(std::integral_constant<int, 0>(), kc);
+      load_a(kc, 0);
+      write_a(smem, 0, 0, 8);
+      load_a(kc, 1);
+      write_a(smem, 1, 0, 8);
+      __syncthreads();
+      read_a(smem, 0, 0);
+      convert_b_scales(std::integral_constant<int, 0>());
+      expand(std::integral_constant<int, 0>(), 0, 0);
+      for (; kc < kcn; kc += 2) {
+        chunk(std::integral_constant<int, 0>(), kc);
+        chunk(std::integral_constant<int, 1>(), kc + 1);
+      }
+    }
+    if (fast_out && m0 + 256 <= g.m && n0 + 256 <= g.n)
+      store_tiles_fast<4, 4>(g, acc, smem + A_STAGE + wave * OUT_STAGE, m0 + wm * 128, n0 + wn * 128, lane, scale);
+    else
+      store_tiles<4, 4>(g, acc, m0 + wm * 128, n0 + wn * 128, lane, scale);
+  }
+}
+
 // ---------------------------------------------------------------- W4A16, up to 1024 tokens
 // bf16 activations against NVFP4 weights when the output is too small to
 // fill the chip with large tiles (the text-encoder linears). A workgroup
@@ -2400,8 +2624,8 @@ __global__ void __launch_bounds__(64 * NW) k_w4a16_splitk(GemmArgs g) {
 // MV = 4 for m <= 8, 8 for m <= 16. Lanes of activation rows past m read
 // an extra all-zero row. Requires m <= 16 and (m + 1) rows within the LDS
 // budget (checked by the launcher).
-template <int D, int MV>
-__global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
+template <int D, int MV, int NWV = 8>
+__global__ void __launch_bounds__(64 * NWV) k_w4a16_stream(GemmArgs g) {
   constexpr uint32_t OOB = 0x80000000u;
   extern __shared__ __attribute__((aligned(16))) uint8_t xl[];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -2412,7 +2636,7 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
   // stage the activation rows and one zero row (16 bytes per thread and step)
   {
     const int pieces = g.k >> 3;  // 16-byte pieces per row
-    for (int t = threadIdx.x; t < (g.m + 1) * pieces; t += 512) {
+    for (int t = threadIdx.x; t < (g.m + 1) * pieces; t += 64 * NWV) {
       const int row = t / pieces, c = t - row * pieces;
       *reinterpret_cast<uint4*>(xl + row * pitch + c * 16) =
           (row < g.m) ? *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(g.a) + (int64_t)row * g.lda + 8 * c)
@@ -2476,8 +2700,8 @@ __global__ void __launch_bounds__(512) k_w4a16_stream(GemmArgs g) {
       }
     }
   };
-  const int nw = gridDim.x * 8;
-  int panel = blockIdx.x * 8 + wave;
+  const int nw = gridDim.x * NWV;
+  int panel = blockIdx.x * NWV + wave;
   int kc0 = 0, cur = 0;
   if (panel < npan) load(buf[0], panel, 0);
   while (panel < npan) {
@@ -2764,6 +2988,17 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
       const unsigned grid = (unsigned)(((npan_all + ppw - 1) / ppw + 7) / 8);
       if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<4, 4>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
       else hipLaunchKernelGGL((k_w4a16_stream<4, 8>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      return hipGetLastError();
+    }
+    // Past the ridge point with enough 256 x 256 tiles for half a round: the
+    // persistent W4A4-shaped kernel (the weight pool at M = 256, 512: 1.5x the
+    // 128 x 256 tile kernel, which was itself 1.5x the split-K kernels there)
+    const int t256_m = (int)((m + 255) / 256), t256_n = (int)((n + 255) / 256);
+    const int64_t t256 = (int64_t)t256_m * t256_n;
+    if (m > 128 && 2 * t256 >= device_cus()) {
+      g.tiles_m = t256_m;
+      g.tiles_n = t256_n;
+      hipLaunchKernelGGL(k_gemm_w4a16_direct, dim3((unsigned)std::min<int64_t>(t256, device_cus())), dim3(256), 0, st, g);
       return hipGetLastError();
     }
     if (m <= 1024) {

@@ -276,6 +276,27 @@ def test_w4a16_one_row_wide_weight(out):
     log("  max err/B", check_linear(y, oracle.linear_reference("w4a16", x, w)))
 
 
+@pytest.mark.parametrize("m,n,k,out", [(256, 65536, 1024, q.QG_OUT_BF16), (300, 16400, 1152, q.QG_OUT_F32),
+                                       (4608, 3072, 3072, q.QG_OUT_BF16), (1000, 8208, 640, q.QG_OUT_BF16)])
+def test_w4a16_many_tiles_sampled(m, n, k, out):
+    # W4A16 past the ridge point with enough 256 x 256 tiles for the
+    # persistent kernel: a pool-like wide weight, ragged rows and columns
+    # (300, 1000 rows; 16400, 8208 columns), odd chunk counts (K = 1152, 640),
+    # bf16 and fp32 outputs; heavy-tailed activations with subnormal and zero
+    # blocks in some rows
+    log("w4a16 many tiles %dx%dx%d out=%d" % (m, n, k, out))
+    x = synth.normal_bf16(m, k, 1.0, 12, 0, synth.HEAVY_TAIL_FRAC, synth.HEAVY_TAIL_GAIN)
+    x[1, 16:32] &= 0x807F
+    x[2, 32:48] = 0
+    w = synth.normal_bf16(n, k, 0.02, 12, 1)
+    y = run_linear("w4a16", x, w, out, check_codes=False)
+    rows, cols = _sample(m, n, 2000, 13)
+    rows = np.concatenate([rows, [1, 2, m - 1], np.resize(np.arange(255, m, 256), 64)])
+    cols = np.concatenate([cols, [0, n - 1, n // 2], np.resize(np.arange(n - 64, n), 64)])
+    ref = oracle.linear_reference("w4a16", x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))
+
+
 @pytest.mark.parametrize("kind", ["fp8", "nvfp4"])
 def test_linear_with_calibrated_activation_scale(kind):
     # static activation scale calibrated on other batches (the max of their

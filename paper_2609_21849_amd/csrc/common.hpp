@@ -124,15 +124,14 @@ __device__ inline float dec_e4m3_scale(uint32_t c) {
 }
 
 // Four E4M3 block scales (one dword, block b in byte b; never negative) to
-// fp16, exact: the E4M3 bit pattern shifted into the fp16 field is the value
-// divided by 2^8 (normal and subnormal alike), and the multiply by 2^8 lands
-// in the fp16 normal range. Result: .x = blocks 0 and 1, .y = blocks 2 and 3.
+// fp16, exact: every E4M3 value, the subnormal ones included, is a normal
+// fp16 number, and the hardware conversion at unit scale
+// (v_cvt_scalef32_pk_f16_fp8, two codes per instruction) keeps it (checked on
+// every code in every byte position on the GPU). Result: .x = blocks 0 and 1,
+// .y = blocks 2 and 3.
 __device__ __attribute__((always_inline)) inline uint2 e4m3x4_to_f16x4(uint32_t d) {
-  const v2h k256 = {(_Float16)256.0f, (_Float16)256.0f};
-  const uint32_t lo = ((d & 0x7Fu) << 7) | ((d & 0x7F00u) << 15);
-  const uint32_t hi = ((d & 0x7F0000u) >> 9) | ((d & 0x7F000000u) >> 1);
-  return make_uint2(__builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, lo) * k256),
-                    __builtin_bit_cast(uint32_t, __builtin_bit_cast(v2h, hi) * k256));
+  return make_uint2(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d, 1.0f, false)),
+                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d, 1.0f, true)));
 }
 
 // fp16 block scale b (0..3) of a lane's four.

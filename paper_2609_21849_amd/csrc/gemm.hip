@@ -205,15 +205,6 @@ __device__ inline v8h dequant8_f16(uint32_t w, _Float16 sc) {
   return (v8h){p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
 }
 
-// The same with the scale already in both halves of a register.
-__device__ __attribute__((always_inline)) inline v8h dequant8_f16x2(uint32_t w, v2h s2) {
-  const v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0) * s2;
-  const v2h p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1) * s2;
-  const v2h p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2) * s2;
-  const v2h p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3) * s2;
-  return (v8h){p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
-}
-
 // 8 E2M1 codes times an fp32 block scale -> 8 bf16 (exact, so the top half
 // of the fp32 product is already the bf16 value): one conversion, two
 // multiplies and one byte permute per pair.
@@ -727,20 +718,22 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   const int kcn = g.k >> 7;
   const int npanels_w = (g.n + 31) >> 5;
 
-  const __amdgpu_buffer_rsrc_t rs_w = __builtin_amdgcn_make_buffer_rsrc(
+  const __amdgpu_buffer_rsrc_t rs_w_ = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_codes), 0, (int)((int64_t)npanels_w * kcn * (MODE == MODE_FP8 ? 4096 : 2048)), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rs_ws = __builtin_amdgcn_make_buffer_rsrc(
+  const __amdgpu_buffer_rsrc_t rs_ws_ = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.w_scales), 0, MODE == MODE_NVFP4 ? (int)((int64_t)npanels_w * kcn * 256) : 0, 0x00020000);
   // NVFP4 activation rows: lda / 2 code bytes and lda / 16 scale bytes apart,
   // the descriptors ending at the last row's k / 2 and k / 16 bytes
   const int64_t ka = g.lda >> 1, ks = g.lda >> 4;
-  const __amdgpu_buffer_rsrc_t rs_a = (MODE == MODE_FP8)
+  const __amdgpu_buffer_rsrc_t rs_a_ = (MODE == MODE_FP8)
       ? rsrc_a_fp8(g)
       : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)((int64_t)(g.m - 1) * ka + (g.k >> 1)),
                                           0x00020000);
-  const __amdgpu_buffer_rsrc_t rs_as = __builtin_amdgcn_make_buffer_rsrc(
+  const __amdgpu_buffer_rsrc_t rs_as_ = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(g.a_bscale), 0, MODE == MODE_NVFP4 ? (int)((int64_t)(g.m - 1) * ks + (g.k >> 4)) : 0,
       0x00020000);
+
+  const __amdgpu_buffer_rsrc_t rs_none = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.w_codes), 0, 0, 0x00020000);
 
   // per-lane base offsets (rows and panels outside the operands: out of range, zeros)
   uint32_t oa[MT], oas[MT], ow[NP], ows[NP];
@@ -773,32 +766,39 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
     uint32_t ws[MODE == MODE_NVFP4 ? NP : 1];
   };
   auto load = [&](Chunk& C, int kc) __attribute__((always_inline)) {
-    const uint32_t hi = kc < kcn ? 0u : OOB;
+    // the chunk's byte offset is uniform (the wave index is scalar), so it
+    // travels in the loads' scalar offset; loads past the last chunk (never
+    // multiplied) go through descriptors of zero bytes, which return zeros
+    // without touching memory
+    const bool in = kc < kcn;
+    const int kq = in ? kc : 0;
+    const __amdgpu_buffer_rsrc_t rs_a = in ? rs_a_ : rs_none, rs_as = in ? rs_as_ : rs_none;
+    const __amdgpu_buffer_rsrc_t rs_w = in ? rs_w_ : rs_none, rs_ws = in ? rs_ws_ : rs_none;
     if (MODE == MODE_FP8) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {  // step p / 2, register half p % 2
 #pragma unroll
         for (int i = 0; i < MT; ++i)
-          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[i] + kc * 128 + (p >> 1) * 64 + (p & 1) * 16) | hi, 0, 0);
+          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + (p >> 1) * 64 + (p & 1) * 16, kq * 128, 0);
 #pragma unroll
         for (int j = 0; j < NP; ++j)
-          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 4096 + p * 1024) | hi, 0, 0);
+          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, ow[j] + p * 1024, kq * 4096, 0);
       }
     } else {
       // in the order of use: block scales, then code halves 0 (steps 0..3)
       // and 1 (steps 4..7), so each step waits only for what it reads
 #pragma unroll
-      for (int i = 0; i < MT; ++i) C.as[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_as, (oas[i] + kc * 8) | hi, 0, 0);
+      for (int i = 0; i < MT; ++i) C.as[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_as, oas[i], kq * 8, 0);
 #pragma unroll
-      for (int j = 0; j < NP; ++j) C.ws[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, (ows[j] + kc * 256) | hi, 0, 0);
+      for (int j = 0; j < NP; ++j) C.ws[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_ws, ows[j], kq * 256, 0);
 #pragma unroll
       for (int p = 0; p < 2; ++p) {
 #pragma unroll
         for (int i = 0; i < MT; ++i)
-          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, (oa[i] + kc * 64 + 16 * p) | hi, 0, 0);
+          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + 16 * p, kq * 64, 0);
 #pragma unroll
         for (int j = 0; j < NP; ++j)
-          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, (ow[j] + kc * 2048 + 1024 * p) | hi, 0, 0);
+          C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, ow[j] + 1024 * p, kq * 2048, 0);
       }
     }
     // keep each chunk's loads together and in this order: the waits before
@@ -836,19 +836,13 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
             acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[j], fa[i], acc[i][j], 0, 0, 0, 0, 0, 0);
       }
     } else {
-      // the lane's four block scales as fp16, each in both halves of a register
-      v2h sa[MT][4], sw[NP][4];
-      auto dup = [&](uint32_t d, v2h (&o)[4]) __attribute__((always_inline)) {
-        const uint2 h = e4m3x4_to_f16x4(d);
-        o[0] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.x, h.x, 0x05040504u));
-        o[1] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.x, h.x, 0x07060706u));
-        o[2] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.y, h.y, 0x05040504u));
-        o[3] = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(h.y, h.y, 0x07060706u));
-      };
+      // the lane's four block scales as fp16 (the multiplies take the one
+      // they need from its register half)
+      uint2 sa[MT], sw[NP];
 #pragma unroll
-      for (int i = 0; i < MT; ++i) dup(C.as[i], sa[i]);
+      for (int i = 0; i < MT; ++i) sa[i] = e4m3x4_to_f16x4(C.as[i]);
 #pragma unroll
-      for (int j = 0; j < NP; ++j) dup(C.ws[j], sw[j]);
+      for (int j = 0; j < NP; ++j) sw[j] = e4m3x4_to_f16x4(C.ws[j]);
       // step s: elements [64 g + 8 s, +8) of the chunk, block 4 g + s / 2;
       // the expansion of step s + 1 is issued between the MFMAs of step s
       v8h fa[2][MT], fb[2][NP];
@@ -857,13 +851,13 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
         for (int i = 0; i < MT; ++i) {
           const v4i c = C.a[i][s >> 2];
           const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
-          fa[set][i] = dequant8_f16x2(w, sa[i][s >> 1]);
+          fa[set][i] = dequant8_f16(w, scale_f16(sa[i], s >> 1));
         }
 #pragma unroll
         for (int j = 0; j < NP; ++j) {
           const v4i c = C.w[j][s >> 2];
           const uint32_t w = (uint32_t)((s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w);
-          fb[set][j] = dequant8_f16x2(w, sw[j][s >> 1]);
+          fb[set][j] = dequant8_f16(w, scale_f16(sw[j], s >> 1));
         }
       };
       expand(0, 0);

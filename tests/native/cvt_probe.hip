@@ -80,7 +80,7 @@ __global__ void k_probe_f16_scale(uint16_t* out) {
 //   f32[4 c + b] = v_cvt_pk_f32_fp8 (hardware, the W4A16 weight-pool kernels),
 //   and, for c < 128 (block scales are magnitudes),
 //   ref[4 c + b] = dec_e4m3_scale (the W4A16 split-K kernel),
-//   h16[4 c + b] = e4m3x4_to_f16x4 (the W4A4 kernels).
+//   h16[4 c + b] = e4m3x4_to_f16x4 (the W4A4 kernels; v_cvt_scalef32_pk_f16_fp8).
 __global__ void k_probe_scale_decoders(float* f32, float* ref, uint16_t* h16) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 256 * 4) return;

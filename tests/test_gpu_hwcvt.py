@@ -49,12 +49,12 @@ def test_f16_conversion_of_e2m1_is_exact_at_unit_scale():
 def test_block_scale_decoders_on_every_code():
     """The E4M3 block-scale decoders the GEMM kernels use, on every code and
     in every byte position, against the oracle's E4M3 table: the hardware
-    v_cvt_pk_f32_fp8 (W4A16 weight-pool kernels) on all 256 codes (the two
-    NaN codes give NaN), and on the 128 non-negative codes (block scales are
-    magnitudes) the bit-move decoders of the split-K W4A16 kernel (fp32) and
-    of the W4A4 kernels (fp16, four per dword). The E4M3 subnormal codes 1..7
-    become fp32 and fp16 subnormals on the way, so this pins the denormal
-    handling too."""
+    v_cvt_pk_f32_fp8 (W4A16 weight-pool and large-M kernels) on all 256 codes
+    (the two NaN codes give NaN), and on the 128 non-negative codes (block
+    scales are magnitudes) the bit-move decoder of the split-K W4A16 kernel
+    (fp32; the E4M3 subnormal codes 1..7 pass through fp32 subnormals) and the
+    hardware v_cvt_scalef32_pk_f16_fp8 at unit scale of the W4A4 kernels (fp16,
+    four per dword)."""
     L = _probe()
     f32 = torch.full((1024,), 12345.0, dtype=torch.float32, device="cuda")
     ref = torch.full((1024,), 12345.0, dtype=torch.float32, device="cuda")

@@ -51,6 +51,9 @@ def parse():
                     help="turn the two counter runs of --traffic-probe into the traffic summary")
     ap.add_argument("--mfma-summary", nargs=2, metavar=("PMC_DIR", "OUT_MD"),
                     help="turn a MfmaUtil counter run of --traffic-probe into the MFMA-utilisation summary")
+    ap.add_argument("--stall-summary", nargs=2, metavar=("PMC_DIRS", "OUT_MD"),
+                    help="turn the counter passes STALL_PASSES over --traffic-probe (directories comma-separated) "
+                         "into the wave-time summary")
     ap.add_argument("--kind", choices=("nvfp4", "fp8"), default="nvfp4",
                     help="format of the --traffic-summary / --mfma-summary counter runs")
     ap.add_argument("--w4a16-pool-only", action="store_true",
@@ -62,8 +65,16 @@ def parse():
 # --traffic-probe / --traffic-summary) and kept as a text summary; reported
 # only while the kernel source is the one the counters were taken on.
 TRAFFIC_MD = {"nvfp4": os.path.join(ROOT, "profiles", "k_gemm_nvfp4_direct_dit_traffic.md"),
-              "fp8": os.path.join(ROOT, "profiles", "k_gemm_fp8_direct_dit_traffic.md")}
-KERNEL = {"nvfp4": "k_gemm_nvfp4_direct", "fp8": "k_gemm_fp8_direct"}
+              "fp8": os.path.join(ROOT, "profiles", "k_gemm_fp8_t288_dit_traffic.md")}
+KERNEL = {"nvfp4": "k_gemm_nvfp4_direct", "fp8": "k_gemm_fp8_t288"}
+# counter passes of --stall-summary (each within one pass's per-block counter limits)
+STALL_PASSES = (
+    "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
+    "SQ_VALU_MFMA_COEXEC_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA GRBM_GUI_ACTIVE",
+    "SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VMEM SQ_WAIT_INST_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS SQ_ACTIVE_INST_SCA "
+    "TA_BUSY_avr TA_DATA_STALLED_BY_TC_CYCLES",
+    "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_READ_REQ_sum TCP_PENDING_STALL_CYCLES_sum TCP_TCR_TCP_STALL_CYCLES_sum "
+    "TCC_HIT_sum TCC_MISS_sum")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_21849_amd", "csrc", "gemm.hip")
 COPY_BYTES = 512 * 2 ** 20
 
@@ -215,6 +226,86 @@ def traffic_summary(fetch_dir, write_dir, out_md, kind="nvfp4"):
     print(json.dumps(data))
 
 
+def stall_summary(pmc_dirs, out_md, kind):
+    """Where a DiT GEMM kernel's waves spend their time, from the counter
+    passes STALL_PASSES over --traffic-probe (one rocprofv3 run per pass, in
+    the directories pmc_dirs, comma-separated): per shape, the mean over the
+    second and third launch."""
+    import csv
+    import glob
+    import synth
+    kern = KERNEL[kind]
+    per = {}   # dispatch -> {counter: value, "ns": duration}
+    for d in pmc_dirs.split(","):
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if kern not in r["Kernel_Name"]:
+                    continue
+                key = (d, int(r["Dispatch_Id"]))
+                e = per.setdefault(key, {})
+                e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                e["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    by_dir = {}
+    for (d, disp), e in sorted(per.items()):
+        by_dir.setdefault(d, []).append(e)
+    shapes = list(synth.DIT_LINEARS.items())
+    M = synth.DIT_TOKENS
+    rows = []
+    for i, (name, (n, k)) in enumerate(shapes):
+        v, ns = {}, []
+        for d, launches in by_dir.items():
+            assert len(launches) == 12, (d, len(launches))
+            for e in launches[3 * i + 1:3 * i + 3]:
+                ns.append(e["ns"])
+                for c, x in e.items():
+                    if c != "ns":
+                        v.setdefault(c, []).append(x)
+        v = {c: sum(x) / len(x) for c, x in v.items()}
+        wave = 4.0 * v["SQ_WAVE_CYCLES"]          # wave-cycles (the counter counts quad-cycles)
+        rows.append((name, n, k, {
+            "clock_ghz": v["GRBM_GUI_ACTIVE"] / 8 / (sum(ns) / len(ns)),
+            "mfma_busy_of_wave": v["SQ_VALU_MFMA_BUSY_CYCLES"] / wave,
+            "coexec_of_mfma": v["SQ_VALU_MFMA_COEXEC_CYCLES"] / v["SQ_VALU_MFMA_BUSY_CYCLES"],
+            "wait_any_of_wave": v["SQ_WAIT_ANY"] / v["SQ_WAVE_CYCLES"],
+            "wait_issue_of_wave": v["SQ_WAIT_INST_ANY"] / v["SQ_WAVE_CYCLES"],
+            "wait_lds_of_wave": v["SQ_WAIT_INST_LDS"] / v["SQ_WAVE_CYCLES"],
+            "valu_per_mfma": (v["SQ_INSTS_VALU"] - v["SQ_INSTS_MFMA"]) / v["SQ_INSTS_MFMA"],
+            "lds_conflict_per_lds_inst": v["SQ_LDS_BANK_CONFLICT"] / v["SQ_INSTS_LDS"],
+            "l2_hit": v["TCC_HIT_sum"] / (v["TCC_HIT_sum"] + v["TCC_MISS_sum"]),
+            "l2_read_latency_cycles": v["TCP_TCC_READ_REQ_LATENCY_sum"] / v["TCP_TCC_READ_REQ_sum"],
+            "wave_life_of_kernel": wave / (v["GRBM_GUI_ACTIVE"] / 8) / (4 * 256)}))
+    cmds = ["cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc %s --output-format csv "
+            "-d gpurun_out/pmc_stall_%s_%d -o run -- python3 bench.py --traffic-probe %s" % (p, kind, j + 1, kind)
+            for j, p in enumerate(STALL_PASSES)]
+    cmds.append("python3 bench.py --stall-summary %s <this file> --kind %s"
+                % (",".join("gpurun_out/pmc_stall_%s_%d" % (kind, j + 1) for j in range(len(STALL_PASSES))), kind))
+    cols = [("clock_ghz", "clock (GHz)", "%.2f"), ("wave_life_of_kernel", "wave life / kernel", "%.2f"),
+            ("mfma_busy_of_wave", "MFMA busy / wave life", "%.2f"), ("coexec_of_mfma", "VALU co-issue / MFMA busy", "%.2f"),
+            ("wait_any_of_wave", "waiting (waitcnt, barrier) / wave life", "%.2f"),
+            ("wait_issue_of_wave", "waiting to issue / wave life", "%.2f"),
+            ("wait_lds_of_wave", "waiting to issue LDS / wave life", "%.3f"),
+            ("valu_per_mfma", "VALU instr. per MFMA", "%.2f"),
+            ("lds_conflict_per_lds_inst", "LDS bank-conflict cycles per LDS instr.", "%.2f"),
+            ("l2_hit", "L2 hit rate", "%.3f"), ("l2_read_latency_cycles", "L1->L2 read latency (cycles)", "%.0f")]
+    lines = ["# Where the waves of `%s` spend their time (transformer shapes, M = %d)" % (kern, M), "",
+             "rocprofv3 counters over `bench.py --traffic-probe %s` (each DiT-shaped GEMM launched three times; "
+             "the mean of launches 2 and 3 per shape), %d counter passes. Ratios: wave-cycles = 4 x "
+             "SQ_WAVE_CYCLES (quad-cycles), matrix-pipe busy = SQ_VALU_MFMA_BUSY_CYCLES (one wave per SIMD, so "
+             "per wave), waiting = SQ_WAIT_ANY and SQ_WAIT_INST_ANY (quad-cycles) over SQ_WAVE_CYCLES, VALU "
+             "instructions per MFMA = (SQ_INSTS_VALU - SQ_INSTS_MFMA) / SQ_INSTS_MFMA, clock = GRBM_GUI_ACTIVE "
+             "per XCD over the dispatch's duration, wave life / kernel = wave-cycles over (1024 waves x "
+             "GUI-active cycles per XCD)." % (kind, len(STALL_PASSES)), "",
+             "Commands (repo root, MI355X):", "", "```"] + cmds + ["```", "",
+             "| linear (M x N x K) | " + " | ".join(c[1] for c in cols) + " |",
+             "|---|" + "---:|" * len(cols)]
+    for name, n, k, d in rows:
+        lines.append("| %s (%dx%dx%d) | " % (name, M, n, k) + " | ".join(f % d[c] for c, _, f in cols) + " |")
+    lines += ["", "Source: paper_2609_21849_amd/csrc/gemm.hip, SHA-256 prefix %s." % source_sha(), ""]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def recorded_traffic(kind):
     """(bytes per launch, summary) of the committed traffic summary of the
     `kind` DiT GEMM, or (None, reason) when it is missing or was taken on
@@ -241,6 +332,9 @@ def main():
         return
     if args.mfma_summary:
         mfma_summary(*args.mfma_summary, kind=args.kind)
+        return
+    if args.stall_summary:
+        stall_summary(*args.stall_summary, kind=args.kind)
         return
     if args.traffic_probe:
         traffic_probe(args.traffic_probe)

@@ -2916,10 +2916,23 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     g.tiles_m = (g.m + 255) / 256;
     g.tiles_n = (g.n + 255) / 256;
     const int tiles = g.tiles_m * g.tiles_n;
-    // Few tokens: the split-K kernel on 32 x 64 tiles while those number at
-    // most two per CU (measured at the encoder shapes, M = 16 .. 512: 1.2-1.9x
-    // faster than the 64 x 128 kernel where K >= 3072, equal at K = 1024 up
-    // to 256 rows, slower beyond).
+    // Few tokens: the split-K kernel. FP8 operands need no expansion, so
+    // narrow tiles cost nothing extra: the narrowest 32-row tile (32 x 32 NP,
+    // NP = 1 .. 4) that still gives every workgroup a CU of its own, with
+    // eight waves and one chunk in flight each (NP = 2: four waves, two
+    // chunks); else 32 x 64 tiles while those number at most two per CU.
+    // Measured at M = 16 .. 1024, N, K in {256, 1024, 3072, 9216} (GPU time
+    // from graph replays): the best of five tilings within 2% at every shape
+    // (128 x 256 x 256 3.8 -> 3.2 us, 256 x 3072 x 1024 6.6 -> 5.7 us,
+    // 1024 x 1024 x 3072 11.9 -> 10.0 us; the 32 x 64 rule alone was 1.2-1.9x
+    // faster than the 64 x 128 kernel where K >= 3072).
+    if (m <= 1024) {
+      const int64_t rows32 = (m + 31) / 32;
+      if (rows32 * ((n + 31) / 32) <= cus) return run_splitk<MODE_FP8, 1, 1, 8, 1>(g, st);
+      if (rows32 * ((n + 63) / 64) <= cus) return run_splitk<MODE_FP8, 1, 2, 4, 2>(g, st);
+      if (rows32 * ((n + 95) / 96) <= cus) return run_splitk<MODE_FP8, 1, 3, 8, 1>(g, st);
+      if (rows32 * ((n + 127) / 128) <= cus) return run_splitk<MODE_FP8, 1, 4, 8, 1>(g, st);
+    }
     const int64_t small_tiles = (int64_t)((m + 31) / 32) * ((n + 63) / 64);
     if (small_tiles <= 2 * cus) return run_splitk<MODE_FP8, 1, 2, 4, 2>(g, st);
     // Too few 256 x 256 tiles to fill the chip: the 64 x 128 kernel's eight

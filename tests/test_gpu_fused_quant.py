@@ -32,7 +32,8 @@ def run(kind, x, w, s_y):
 
 
 @pytest.mark.parametrize("kind", list(KINDS))
-@pytest.mark.parametrize("m,n,k", [(1, 16, 256), (37, 80, 512), (300, 272, 768), (129, 528, 1280)])
+@pytest.mark.parametrize("m,n,k", [(1, 16, 256), (37, 80, 512), (300, 272, 768), (129, 528, 1280),
+                                   (250, 2992, 768)])
 @pytest.mark.parametrize("sat", [1.0, 0.25])
 def test_fp8_output_within_contract(kind, m, n, k, sat):
     log("gemm_quant %s m=%d n=%d k=%d sat=%.2f" % (kind, m, n, k, sat))
@@ -107,7 +108,8 @@ def _nv_scale(ref, sat):
 
 
 @pytest.mark.parametrize("kind", NV_KINDS)
-@pytest.mark.parametrize("m,n,k", [(1, 16, 256), (37, 80, 512), (300, 272, 768), (129, 528, 1280)])
+@pytest.mark.parametrize("m,n,k", [(1, 16, 256), (37, 80, 512), (300, 272, 768), (129, 528, 1280),
+                                   (250, 2992, 768)])
 @pytest.mark.parametrize("sat", [1.0, 0.25])
 def test_nvfp4_output_within_contract(kind, m, n, k, sat):
     log("gemm_quant_nvfp4 %s m=%d n=%d k=%d sat=%.2f" % (kind, m, n, k, sat))

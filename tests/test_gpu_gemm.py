@@ -200,11 +200,13 @@ def test_dit_linear_sampled(kind, name):
 
 @pytest.mark.parametrize("kind", ["fp8", "nvfp4"])
 @pytest.mark.parametrize("m,n,k", [(256, 3072, 1024), (512, 1024, 3072), (2048, 1024, 3072), (1530, 3072, 3072),
-                                   (2300, 3072, 3072), (3072, 3072, 1024)])
+                                   (2300, 3072, 3072), (3072, 3072, 1024), (1000, 1008, 1152), (250, 2992, 768)])
 def test_mid_m_linear_sampled(kind, m, n, k):
     # token counts between the small-M shapes and the transformer's (ragged
     # ones among them), on both sides of the tile-count thresholds that pick
-    # the 64 x 128 kernels (FP8, W4A4) over the persistent 256 x 256 ones
+    # the 64 x 128 kernels (FP8, W4A4) over the persistent 256 x 256 ones, and
+    # FP8 split-K tilings 32 x 128 (1000 x 1008, nine chunks over eight waves)
+    # and 32 x 96 (250 x 2992, six chunks: two waves without one)
     log("%s mid-m %dx%dx%d" % (kind, m, n, k))
     x = synth.normal_bf16(m, k, 1.0, 7, 0)
     w = synth.normal_bf16(n, k, 0.02, 7, 1)

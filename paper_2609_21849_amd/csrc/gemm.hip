@@ -2696,18 +2696,20 @@ __global__ void __launch_bounds__(64 * NWV) k_w4a16_stream(GemmArgs g) {
   };
   const int nw = gridDim.x * NWV;
   int panel = blockIdx.x * NWV + wave;
-  int kc0 = 0, cur = 0;
-  if (panel < npan) load(buf[0], panel, 0);
-  while (panel < npan) {
+  int kc0 = 0;
+  // one group of D chunks: load the group after it into nb while computing cb;
+  // false once the wave has no panel left. The loop below alternates the two
+  // register sets in straight-line code (a runtime set index made the
+  // compiler copy the loaded sets around every iteration).
+  auto group = [&](W (&cb)[D], W (&nb)[D]) __attribute__((always_inline)) {
     // the group after this one: next chunks of this panel, or the next panel
     int np_ = panel, nk = kc0 + D;
     if (nk >= kcn) { np_ = panel + nw; nk = 0; }
     if (kc0 == 0)
 #pragma unroll
       for (int v = 0; v < MV; ++v) acc[v] = 0.0f;
-    if (cur == 0) { load(buf[1], np_, nk); compute(buf[0], kc0); }
-    else { load(buf[0], np_, nk); compute(buf[1], kc0); }
-    cur ^= 1;
+    load(nb, np_, nk);
+    compute(cb, kc0);
     if (nk == 0) {
       // panel done: lane (r, g) holds column n = 32 panel + r of rows 8 (v / 4) + 4 g + v % 4
       const int n = panel * 32 + r;
@@ -2724,6 +2726,12 @@ __global__ void __launch_bounds__(64 * NWV) k_w4a16_stream(GemmArgs g) {
     }
     panel = np_;
     kc0 = nk;
+    return panel < npan;
+  };
+  if (panel < npan) load(buf[0], panel, 0);
+  while (panel < npan) {
+    if (!group(buf[0], buf[1])) break;
+    group(buf[1], buf[0]);
   }
 }
 

@@ -2997,12 +2997,17 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
       return hipGetLastError();
     }
     if (m <= 16 && npan_all >= 8 * (int64_t)device_cus() && xbytes <= 128 * 1024 && out_mode != OUT_FP8) {
-      // one workgroup per CU, balanced like the matrix-vector kernel's grid
-      const int64_t wmax = 8 * (int64_t)device_cus();
+      // one workgroup per CU (the activation rows take most of the LDS),
+      // balanced like the matrix-vector kernel's grid; as many waves as the
+      // registers allow without spills: 16 waves with two chunks in flight at
+      // M <= 8, 12 waves with three at M <= 16 (3-4% / 1% faster than 8 waves
+      // with four on the cold pool)
+      const int nwv = m <= 8 ? 16 : 12;
+      const int64_t wmax = nwv * (int64_t)device_cus();
       const int64_t ppw = (npan_all + wmax - 1) / wmax;
-      const unsigned grid = (unsigned)(((npan_all + ppw - 1) / ppw + 7) / 8);
-      if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<4, 4>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
-      else hipLaunchKernelGGL((k_w4a16_stream<4, 8>), dim3(grid), dim3(512), (size_t)xbytes, st, g);
+      const unsigned grid = (unsigned)(((npan_all + ppw - 1) / ppw + nwv - 1) / nwv);
+      if (m <= 8) hipLaunchKernelGGL((k_w4a16_stream<2, 4, 16>), dim3(grid), dim3(1024), (size_t)xbytes, st, g);
+      else hipLaunchKernelGGL((k_w4a16_stream<3, 8, 12>), dim3(grid), dim3(768), (size_t)xbytes, st, g);
       return hipGetLastError();
     }
     // Past the ridge point with enough 256 x 256 tiles for half a round: the

@@ -54,8 +54,10 @@ def test_fp8_output_within_contract(kind, m, n, k, sat):
     assert np.array_equal(codes, want)
 
 
-@pytest.mark.parametrize("kind", ["fp8", "nvfp4", "mxfp4"])
+@pytest.mark.parametrize("kind", ["fp8", "nvfp4", "mxfp4", "w4a16"])
 def test_fp8_output_transformer_shape_sampled(kind):
+    # the persistent large-M kernel of each format (W8A8: 288 x 192 tiles;
+    # W4A16: the bf16 kernel past the ridge point) writing FP8 codes
     m, (n, k) = synth.DIT_TOKENS, synth.DIT_LINEARS["qkv"]
     x = synth.normal_bf16(m, k, 1.0, 0, 0)
     w = synth.normal_bf16(n, k, 0.02, 0, 1)

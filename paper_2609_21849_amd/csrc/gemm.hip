@@ -1705,9 +1705,11 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp8_direct(GemmArgs g) {
 //                 converted to fp16 once per workgroup while staging);
 //   expansion   : software-pipelined one step ahead of the MFMAs that use it,
 //                 into two sets of fp16 fragments.
-// One barrier per chunk, after step 6; step 7 reads the next chunk's first
-// activation fragments. Persistent grid and staged epilogue as in
-// k_gemm_fp8_direct.
+// One barrier per chunk, after step 5 (the next chunk's staging writes are
+// issued at steps 4 and 5); step 6 reads the next chunk's first activation
+// code half and scales, a whole step before step 7 expands them (read one
+// MFMA before their use, their latency stalled the wave). Persistent grid and
+// staged epilogue as in k_gemm_fp8_direct.
 __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
   constexpr int A_CODES = 8 * 2048;              // 256 rows x 64 B of codes
   constexpr int A_STAGE = A_CODES + 256 * 16;    // + 256 rows x 8 fp16 scales
@@ -1813,14 +1815,15 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[D][j], fa[D][i], acc[i][j], 0, 0, 0);
   };
-  // 16 MFMAs, each followed by its share of the expansion (64 VALU + scale work)
-  auto interleave = [&](int nvmem, int nds_r, int nds_w) __attribute__((always_inline)) {
+  // 16 MFMAs, each followed by its share of the expansion (64 VALU + scale
+  // work); LDS reads in the groups whose bit is set in rmask
+  auto interleave = [&](int nvmem, unsigned rmask, int nds_w) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
       if (t < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      if (t < nds_r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if ((rmask >> t) & 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (t < nds_w) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
     }
   };
@@ -1838,7 +1841,7 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
       if (s == 2) read_a_half(cur, 1);
       mfmas(s & 1);
       expand(Pc, s + 1, (s + 1) & 1);
-      interleave(s == 0 ? 12 : 0, s == 2 ? 4 : 0, 0);
+      interleave(s == 0 ? 12 : 0, s == 2 ? 0xFu : 0u, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     // steps 4, 5: stage the activations of chunk kc + 1, then load kc + 2
@@ -1849,23 +1852,28 @@ __global__ void __launch_bounds__(256) k_gemm_nvfp4_direct(GemmArgs g) {
       if (s == 5) load_a(kc + 2);
       mfmas(s & 1);
       expand(Pc, s + 1, (s + 1) & 1);
-      interleave(s == 5 ? 5 : 0, 0, s == 4 ? 2 : 3);
+      interleave(s == 5 ? 5 : 0, 0u, s == 4 ? 2 : 3);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // step 6, then the barrier that publishes chunk kc + 1
-    mfmas(0);
-    expand(Pc, 7, 1);
-    interleave(0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
+    // the barrier that publishes chunk kc + 1 (its last writes were issued at
+    // the start of step 5)
     __syncthreads();
     __builtin_amdgcn_sched_barrier(0);
-    // step 7 covers the next chunk's first reads and its step-0 expansion
+    // step 6 reads the next chunk's first code half (its ac[0] was last
+    // expanded in step 2) and, once this step's expansion has used the
+    // current scales, the next chunk's scales: a step of MFMAs hides their
+    // latency before step 7 expands them
     read_a_half(nxt, 0);
+    mfmas(0);
+    expand(Pc, 7, 1);
     read_a_scales(nxt);
+    interleave(0, 0x0F0Fu, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // step 7: the next chunk's step-0 expansion
     convert_b_scales(Q);
     mfmas(1);
     expand(Q, 0, 0);
-    interleave(0, 8, 0);
+    interleave(0, 0u, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
 

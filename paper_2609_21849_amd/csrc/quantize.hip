@@ -7,7 +7,9 @@
 // paragraph; Table 2). The same kernels quantize weights offline (PTQ).
 //
 // A tensor-wide scale needs the tensor-wide max before any element can be
-// coded, so one call is a short chain on the caller's stream:
+// coded. A small tensor (at most 3072 units of 16 elements) is quantized by
+// one workgroup in one kernel (k_quant_small); any other is a short chain on
+// the caller's stream:
 //   k_amax_partial : max |x| as an integer max of bf16 magnitude bits (the
 //                    bit pattern of a non-negative value orders like the
 //                    value); one partial per workgroup, parked in the code
@@ -155,7 +157,71 @@ __device__ inline void load16(const uint16_t* p, float (&v)[16]) {
   }
 }
 
+// ---------------------------------------------------------------- units of 16
+// A unit: cnt (<= 16) consecutive bf16 of a row, held as 8 words (element
+// 2 i in the low half of word i, missing elements zero). VEC: the unit is
+// whole and 16-byte aligned (two 16-byte loads).
+template <bool VEC>
+__device__ inline void unit_load(const uint16_t* __restrict__ p, int64_t cnt, uint32_t (&w)[8]) {
+  if (VEC && cnt == 16) {
+    const uint4 a = reinterpret_cast<const uint4*>(p)[0], b = reinterpret_cast<const uint4*>(p)[1];
+    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t lo = (2 * i < cnt) ? (uint32_t)p[2 * i] : 0u;
+      const uint32_t hi = (2 * i + 1 < cnt) ? (uint32_t)p[2 * i + 1] : 0u;
+      w[i] = lo | (hi << 16);
+    }
+  }
+}
+
+// FP8 codes of a unit: q = E4M3(x * r) by the hardware conversion (hw_e4m3x4,
+// equal to enc_e4m3 on every finite input); one 16-byte store when vec_store
+// (whole unit, 16-byte aligned destination), else byte stores.
+__device__ inline void quant_fp8_words(const uint32_t (&w)[8], int64_t cnt, uint8_t* __restrict__ dst, float r,
+                                       bool vec_store) {
+  uint32_t c[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float y[4] = {__fmul_rn(bf16_lo(w[2 * i]), r), __fmul_rn(bf16_hi(w[2 * i]), r),
+                        __fmul_rn(bf16_lo(w[2 * i + 1]), r), __fmul_rn(bf16_hi(w[2 * i + 1]), r)};
+    c[i] = hw_e4m3x4(y);
+  }
+  if (vec_store && cnt == 16) {
+    *reinterpret_cast<uint4*>(dst) = make_uint4(c[0], c[1], c[2], c[3]);
+  } else {
+    for (int64_t i = 0; i < cnt; ++i) dst[i] = (uint8_t)((c[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+  }
+}
+
+// NVFP4 block of a whole unit: block max, E4M3 block scale (returned), then
+// the 16 E2M1 codes packed into 8 bytes at q8 (element 2i in the low nibble;
+// hardware conversion hw_e2m1x8, equal to enc_e2m1 on every input).
+__device__ inline uint32_t quant_nvfp4_words(const uint32_t (&w)[8], uint8_t* __restrict__ q8, float s_t) {
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    v[2 * i] = bf16_lo(w[i]);
+    v[2 * i + 1] = bf16_hi(w[i]);
+  }
+  uint32_t amax_bits = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) amax_bits = max(amax_bits, f2u(v[i]) & 0x7FFFFFFFu);
+  const float d_t = __fmul_rn(6.0f, s_t);
+  const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(amax_bits), d_t) : 0.0f;
+  const uint32_t sb = enc_e4m3(vb);
+  const float S = __fmul_rn(dec_e4m3(sb), s_t);
+  const float r = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
+  float y[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) y[i] = __fmul_rn(v[i], r);
+  *reinterpret_cast<uint2*>(q8) = make_uint2(hw_e2m1x8(y), hw_e2m1x8(y + 8));
+  return sb;
+}
+
 // ---------------------------------------------------------------- FP8
+
 // One thread codes 16 consecutive elements of a row: q = E4M3(x * r), r = 1/s.
 // CONTIG: the tensor is one dense run of n elements (ldx == cols); a thread
 // owns elements [16 t, 16 t + 16) and the last thread may be partial.
@@ -182,25 +248,13 @@ __global__ void __launch_bounds__(256) k_quant_fp8(const uint16_t* __restrict__ 
     dst = row * cols + u * 16;
     cnt = min((int64_t)16, cols - u * 16);
   }
-  if (VEC && cnt == 16) {
-    float v[16];
-    load16<true>(x + src, v);
-    uint32_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[i] = enc_e4m3(__fmul_rn(v[4 * i], r)) | (enc_e4m3(__fmul_rn(v[4 * i + 1], r)) << 8) |
-             (enc_e4m3(__fmul_rn(v[4 * i + 2], r)) << 16) |
-             (enc_e4m3(__fmul_rn(v[4 * i + 3], r)) << 24);
-    *reinterpret_cast<uint4*>(q + dst) = make_uint4(w[0], w[1], w[2], w[3]);
-  } else {
-    for (int64_t i = 0; i < cnt; ++i)
-      q[dst + i] = (uint8_t)enc_e4m3(__fmul_rn(u2f((uint32_t)x[src + i] << 16), r));
-  }
+  uint32_t w[8];
+  unit_load<VEC>(x + src, cnt, w);
+  quant_fp8_words(w, cnt, q + dst, r, VEC);
 }
 
 // ---------------------------------------------------------------- NVFP4
-// One thread per 16-element block: block max, E4M3 block scale, then the 16
-// E2M1 codes packed into 8 bytes (element 2i in the low nibble).
+// One thread per 16-element block.
 template <bool VEC, bool CONTIG>
 __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict__ x, int64_t rows,
                                                      int64_t cols, int64_t ldx,
@@ -218,22 +272,71 @@ __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict_
     if (row >= rows) return;
     src = row * ldx + b * 16;
   }
-  float v[16];
-  load16<VEC>(x + src, v);
-  uint32_t amax_bits = 0;
+  uint32_t w[8];
+  unit_load<VEC>(x + src, 16, w);
+  bscale[t] = (uint8_t)quant_nvfp4_words(w, q + t * 8, *tscale);
+}
+
+// ---------------------------------------------------------------- small tensors
+// The whole dynamic quantization of a small tensor (at most 3072 units of 16
+// elements) in one workgroup: every thread loads its (up to three) units into
+// registers at once, the workgroup reduces the max, and the codes come from
+// the same registers -- one launch and one read instead of the three-kernel
+// chain, whose launch latencies dominate at these sizes. The same arithmetic
+// as the chain, so the same bits: the max of the bf16 magnitude bits,
+// s = fl(amax / 448) or fl(amax / 2688) (NaN if the tensor holds inf or NaN),
+// then the unit helpers above. FP8 rows may end in a shorter unit; NVFP4
+// rows are whole blocks. VEC: 16-byte aligned rows of a multiple of 8
+// elements; vec_store (FP8): 16-byte aligned codes and cols % 16 == 0.
+constexpr int kSmallPerThread = 3;
+constexpr int64_t kSmallUnits = 1024 * kSmallPerThread;
+
+template <int FMT, bool VEC>
+__global__ void __launch_bounds__(1024) k_quant_small(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                      int64_t ldx, uint8_t* __restrict__ q,
+                                                      uint8_t* __restrict__ bscale, float* __restrict__ tscale,
+                                                      bool vec_store) {
+  const int64_t upr = (cols + 15) >> 4;
+  const int64_t units = rows * upr;
+  uint32_t w[kSmallPerThread][8];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) amax_bits = max(amax_bits, f2u(v[i]) & 0x7FFFFFFFu);
-  const float s_t = *tscale;
-  const float d_t = __fmul_rn(6.0f, s_t);
-  const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(amax_bits), d_t) : 0.0f;
-  const uint32_t sb = enc_e4m3(vb);
-  const float S = __fmul_rn(dec_e4m3(sb), s_t);
-  const float r = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
-  uint32_t w[2] = {0u, 0u};
+  for (int i = 0; i < kSmallPerThread; ++i) {
+    const int64_t u = threadIdx.x + 1024 * i;
+    if (u < units) {
+      const int64_t row = u / upr, c = (u - row * upr) * 16;
+      unit_load<VEC>(x + row * ldx + c, min((int64_t)16, cols - c), w[i]);
+    } else {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) w[i >> 3] |= enc_e2m1(__fmul_rn(v[i], r)) << (4 * (i & 7));
-  *reinterpret_cast<uint2*>(q + t * 8) = make_uint2(w[0], w[1]);
-  bscale[t] = (uint8_t)sb;
+      for (int j = 0; j < 8; ++j) w[i][j] = 0u;
+    }
+  }
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < kSmallPerThread; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t t = w[i][j] & 0x7FFF7FFFu;
+      m = max(m, max(t & 0xFFFFu, t >> 16));
+    }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t part[16];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  uint32_t a = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a = max(a, part[i]);
+  a <<= 16;
+  const float s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), FMT == 1 ? 448.0f : 2688.0f);
+  if (threadIdx.x == 0) *tscale = s;
+  const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
+#pragma unroll
+  for (int i = 0; i < kSmallPerThread; ++i) {
+    const int64_t u = threadIdx.x + 1024 * i;
+    if (u >= units) continue;
+    const int64_t row = u / upr, c = (u - row * upr) * 16;
+    if (FMT == 1) quant_fp8_words(w[i], min((int64_t)16, cols - c), q + row * cols + c, r, vec_store);
+    else bscale[u] = (uint8_t)quant_nvfp4_words(w[i], q + u * 8, s);
+  }
 }
 
 // ---------------------------------------------------------------- dense tensors
@@ -546,6 +649,23 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
   }
   const bool contig = (ldx == cols);
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0);
+  if (rows * ((cols + 15) / 16) <= kSmallUnits) {
+    // one workgroup does it all (NVFP4 codes are 8-byte aligned: checked by
+    // the caller). Measured against the chain (GPU time from graph replays):
+    // 1 x 1024 .. 3072 3.4 against 6.2-6.7 us, 128 x 256 5.2 against
+    // 6.5-7.3 us, 16 x 3072 6.2-6.6 against 6.5-7.4 us; at 4096 units
+    // (64 Ki elements) the two were level.
+    const bool rvec = aligned && (cols % 8 == 0) && (contig || ldx % 8 == 0);
+    const bool qvec = (reinterpret_cast<uintptr_t>(codes) % 16 == 0) && (cols % 16 == 0);
+    if (fmt == 1) {
+      if (rvec) hipLaunchKernelGGL((k_quant_small<1, true>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
+      else hipLaunchKernelGGL((k_quant_small<1, false>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
+    } else {
+      if (rvec) hipLaunchKernelGGL((k_quant_small<2, true>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
+      else hipLaunchKernelGGL((k_quant_small<2, false>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
+    }
+    return hipGetLastError();
+  }
   // amax: per-workgroup partial maxima are parked in the code buffer, which
   // the quantize kernel overwrites afterwards (stream order separates them).
   {

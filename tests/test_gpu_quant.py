@@ -47,6 +47,28 @@ def test_fp8_ragged_columns(rows, cols):
 
 
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("rows,cols", [(192, 256), (193, 256), (99, 496), (100, 496), (1, 49152), (3, 16384)])
+def test_small_tensor_path_boundary(fmt, rows, cols):
+    # tensors of up to 3072 units of 16 elements are quantized by one
+    # workgroup in one kernel, larger ones by the three-kernel chain: both
+    # sides of the limit, bit-exact against the oracle
+    x = synth.normal_bf16(rows, cols, 1.0, 8, 0, outlier_frac=0.001, outlier_gain=50.0)
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+
+
+@pytest.mark.parametrize("rows,cols", [(99, 487), (100, 487)])
+def test_small_tensor_path_boundary_ragged_fp8(rows, cols):
+    # FP8 rows that end in a short unit: 99 x 31 units (one workgroup),
+    # 100 x 31 (the chain)
+    x = synth.normal_bf16(rows, cols, 1.0, 9, 0)
+    qt = q.quantize(to_dev_bf16(x), FP8)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
 def test_row_stride_larger_than_row(fmt):
     full = synth.normal_bf16(64, 400, 1.0, 4, 0)
     xd = to_dev_bf16(full)[:, :320]

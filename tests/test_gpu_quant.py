@@ -69,6 +69,19 @@ def test_small_tensor_path_boundary_ragged_fp8(rows, cols):
 
 
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
+@pytest.mark.parametrize("offset", [0, 1])
+def test_strided_rows_past_the_small_limit(fmt, offset):
+    # row stride 1280, 1024 columns, 600 rows (38400 units: the three-kernel
+    # chain's per-row element kernels); offset 1 makes the rows 2-byte aligned
+    # only (the scalar loads)
+    full = synth.normal_bf16(600, 1280, 1.0, 10, 0, outlier_frac=0.001, outlier_gain=50.0)
+    xd = to_dev_bf16(full)[:, offset:offset + 1024]
+    qt = q.quantize(xd, fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, np.ascontiguousarray(full[:, offset:offset + 1024]))
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
 def test_row_stride_larger_than_row(fmt):
     full = synth.normal_bf16(64, 400, 1.0, 4, 0)
     xd = to_dev_bf16(full)[:, :320]

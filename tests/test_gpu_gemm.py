@@ -235,6 +235,28 @@ def test_fp8_whole_round_tiles_sampled(m, n, k, out):
     log("  max err/B", check_linear(y, ref, rows, cols))
 
 
+@pytest.mark.parametrize("m,n,k,out", [(4600, 9200, 3072, q.QG_OUT_BF16), (4608, 3072, 1152, q.QG_OUT_F32),
+                                       (4321, 3056, 640, q.QG_OUT_BF16), (4321, 3056, 640, q.QG_OUT_F32),
+                                       (1000, 8208, 640, q.QG_OUT_BF16)])
+def test_nvfp4_ragged_large_sampled(m, n, k, out):
+    # the persistent 256 x 256 W4A4 kernel at ragged sizes: rows and columns
+    # that leave the last tile row and tile column part-filled (4321, 4600,
+    # 1000 rows; 3056, 9200, 8208 columns, a part-filled last weight panel),
+    # an odd number of 128-wide chunks (K = 1152, 640), bf16 and fp32
+    # outputs, heavy-tailed activations
+    log("nvfp4 ragged %dx%dx%d out=%d" % (m, n, k, out))
+    x = synth.normal_bf16(m, k, 1.0, 11, 0, outlier_frac=0.001, outlier_gain=50.0)
+    w = synth.normal_bf16(n, k, 0.02, 11, 1)
+    y = run_linear("nvfp4", x, w, out, check_codes=False)
+    rows, cols = _sample(m, n, 2000, 12)
+    # the last row, the first row of every tile row and the last column of
+    # every tile column are sampled too
+    rows = np.concatenate([rows, np.full(192, m - 1), np.resize(np.arange(0, m, 256), 192)])
+    cols = np.concatenate([cols, np.arange(n - 192, n), np.resize(np.arange(255, n, 256), 192)])
+    ref = oracle.linear_reference("nvfp4", x, w, rows=rows, cols=cols)
+    log("  max err/B", check_linear(y, ref, rows, cols))
+
+
 @pytest.mark.parametrize("name", list(synth.ENCODER_LINEARS))
 @pytest.mark.parametrize("m", synth.ENCODER_TOKENS)
 def test_w4a16_encoder_full(name, m):

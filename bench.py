@@ -159,11 +159,11 @@ def mfma_summary(pmc_dir, out_md, kind):
              "three times): `MfmaUtil` (SQ_VALU_MFMA_BUSY_CYCLES over the SIMDs / (GRBM_GUI_ACTIVE x SIMD count) x "
              "100), executed MFMA flops (%s%s) and GRBM_GUI_ACTIVE (summed over the 8 XCDs)."
              % (kind, kind.upper(), flops_ctr, " x 512" if kind == "fp8" else ""), "",
-             "Command (repo root, MI355X):", "", "```",
+             "Command (repo root, MI355X; $OUT any output directory):", "", "```",
              "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc MfmaUtil %s "
-             "GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_mfma_%s -o run -- python3 bench.py "
+             "GRBM_GUI_ACTIVE --output-format csv -d $OUT/pmc_mfma_%s -o run -- python3 bench.py "
              "--traffic-probe %s" % (flops_ctr, kind, kind),
-             "python3 bench.py --mfma-summary gpurun_out/pmc_mfma_%s <this file> --kind %s" % (kind, kind), "```", "",
+             "python3 bench.py --mfma-summary $OUT/pmc_mfma_%s <this file> --kind %s" % (kind, kind), "```", "",
              "| linear (M x N x K) | launch | MfmaUtil % | MFMA flops / 2MNK | GUI-active cycles / 8 |",
              "|---|---:|---:|---:|---:|"]
     for i, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
@@ -203,13 +203,13 @@ def traffic_summary(fetch_dir, write_dir, out_md, kind="nvfp4"):
                                  "fetch_factor": round(f_factor, 4), "write_factor": round(w_factor, 4)},
             "per_shape": per}
     lines = ["# HBM traffic of %s at the DiT shapes (M = %d)" % (kern, M), "",
-             "Commands (from the repository root on the MI355X box):", "",
+             "Commands (repo root, MI355X; $OUT any output directory):", "",
              "```",
-             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_%s -o run -- python3 bench.py "
+             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d $OUT/pmc_fetch_%s -o run -- python3 bench.py "
              "--traffic-probe %s" % (kind, kind),
-             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_%s -o run -- python3 bench.py "
+             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d $OUT/pmc_write_%s -o run -- python3 bench.py "
              "--traffic-probe %s" % (kind, kind),
-             "python3 bench.py --traffic-summary gpurun_out/pmc_fetch_%s gpurun_out/pmc_write_%s <this file> --kind %s"
+             "python3 bench.py --traffic-summary $OUT/pmc_fetch_%s $OUT/pmc_write_%s <this file> --kind %s"
              % (kind, kind, kind),
              "```", "",
              "Each counter is scaled by what it reads for a %d MiB device-to-device copy (%d MiB read, %d MiB "
@@ -275,10 +275,10 @@ def stall_summary(pmc_dirs, out_md, kind):
             "l2_read_latency_cycles": v["TCP_TCC_READ_REQ_LATENCY_sum"] / v["TCP_TCC_READ_REQ_sum"],
             "wave_life_of_kernel": wave / (v["GRBM_GUI_ACTIVE"] / 8) / (4 * 256)}))
     cmds = ["cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc %s --output-format csv "
-            "-d gpurun_out/pmc_stall_%s_%d -o run -- python3 bench.py --traffic-probe %s" % (p, kind, j + 1, kind)
+            "-d $OUT/pmc_stall_%s_%d -o run -- python3 bench.py --traffic-probe %s" % (p, kind, j + 1, kind)
             for j, p in enumerate(STALL_PASSES)]
     cmds.append("python3 bench.py --stall-summary %s <this file> --kind %s"
-                % (",".join("gpurun_out/pmc_stall_%s_%d" % (kind, j + 1) for j in range(len(STALL_PASSES))), kind))
+                % (",".join("$OUT/pmc_stall_%s_%d" % (kind, j + 1) for j in range(len(STALL_PASSES))), kind))
     cols = [("clock_ghz", "clock (GHz)", "%.2f"), ("wave_life_of_kernel", "wave life / kernel", "%.2f"),
             ("mfma_busy_of_wave", "MFMA busy / wave life", "%.2f"), ("coexec_of_mfma", "VALU co-issue / MFMA busy", "%.2f"),
             ("wait_any_of_wave", "waiting (waitcnt, barrier) / wave life", "%.2f"),
@@ -295,7 +295,7 @@ def stall_summary(pmc_dirs, out_md, kind):
              "instructions per MFMA = (SQ_INSTS_VALU - SQ_INSTS_MFMA) / SQ_INSTS_MFMA, clock = GRBM_GUI_ACTIVE "
              "per XCD over the dispatch's duration, wave life / kernel = wave-cycles over (1024 waves x "
              "GUI-active cycles per XCD)." % (kind, len(STALL_PASSES)), "",
-             "Commands (repo root, MI355X):", "", "```"] + cmds + ["```", "",
+             "Commands (repo root, MI355X; $OUT any output directory):", "", "```"] + cmds + ["```", "",
              "| linear (M x N x K) | " + " | ".join(c[1] for c in cols) + " |",
              "|---|" + "---:|" * len(cols)]
     for name, n, k, d in rows:

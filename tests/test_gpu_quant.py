@@ -144,9 +144,12 @@ def test_tiny_blocks_get_subnormal_scales():
 
 
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
-def test_nonfinite_input_gives_nan_scale(fmt):
-    x = synth.normal_bf16(4, 64, 1.0, 7, 0)
-    x[2, 9] = 0x7F80  # +inf
+@pytest.mark.parametrize("rows,cols,bad", [(4, 64, 0x7F80), (600, 1024, 0x7F80), (600, 1024, 0xFFC1)])
+def test_nonfinite_input_gives_nan_scale(fmt, rows, cols, bad):
+    # +inf or a NaN anywhere: the single-workgroup kernel (4 x 64) and the
+    # three-kernel chain (600 x 1024) both leave a NaN tensor scale
+    x = synth.normal_bf16(rows, cols, 1.0, 7, 0)
+    x[rows // 2, 9] = bad
     qt = q.quantize(to_dev_bf16(x), fmt)
     torch.cuda.synchronize()
     assert np.isnan(scale_of(qt.tensor_scale))

@@ -107,9 +107,11 @@ typedef enum qg_out_dtype {
  *   block_scales  out: NVFP4 [rows, cols/16] E4M3 bytes; MX [rows, cols/32]
  *                 E8M0 bytes; must be NULL for FP8.
  *   tensor_scale  out: one fp32 decode scale; must be NULL for the MX formats.
- *   The tensor-wide max is reduced in two kernels whose partial results are
- *   parked in `codes` (overwritten by the codes afterwards) or, for tensors
- *   of a few elements, in `tensor_scale`; so x, codes, block_scales and
+ *   A tensor of at most 3072 units of 16 elements (units per row:
+ *   ceil(cols / 16)) is quantized by one single-workgroup kernel. For a
+ *   larger one the tensor-wide max is reduced in two kernels whose partial
+ *   results are parked in `codes` (overwritten by the codes afterwards), then
+ *   a third codes the elements. Either way x, codes, block_scales and
  *   tensor_scale must not overlap.
  *
  * Arithmetic (bit-exact; every step one IEEE binary32 operation, RNE):
@@ -134,8 +136,9 @@ qg_status qg_quantize_act(qg_format fmt, const void *x, int64_t rows, int64_t co
  * qg_quantize_act_static -- quantization of a bf16 tensor with a static
  * (calibrated) decode scale instead of the tensor's own max: post-training
  * quantization with fixed activation ranges, which removes the tensor-wide
- * max reduction (two of the three kernels of qg_quantize_act) from the run
- * time. Paper: Sec. 4, quantization paragraph (PTQ recipe).
+ * max reduction (for all but small tensors, two of the three kernels of
+ * qg_quantize_act) from the run time. Paper: Sec. 4, quantization paragraph
+ * (PTQ recipe).
  *
  *   fmt, x, rows, cols, ldx, codes, block_scales: as for qg_quantize_act.
  *   tensor_scale  in: the fp32 decode scale (FP8: s; NVFP4: s_t), e.g. the

@@ -2230,7 +2230,8 @@ __global__ void __launch_bounds__(256) k_gemm_mxfp4_direct(GemmArgs g) {
 //                 16 lanes that stage one row and the fragment reads of any 8
 //                 or 16 neighbouring lanes fall into distinct bank groups (32
 //                 or 64 banks; checked on the CPU). Staged through registers
-//                 in two batches of eight pieces per thread per chunk.
+//                 in four quarters of four pieces per thread per chunk, two
+//                 register sets, stored at steps 2, 3, 5 and 6.
 // One barrier per chunk, after step 6; step 7 reads the next chunk's first
 // fragments. The bf16 output staging of the epilogue reuses activation
 // stage 1, which no wave reads after the last chunk's barrier (a tile's
@@ -2268,7 +2269,7 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
     la_pair[h] = (uint32_t)(s_c * 1024 + ((((16 * h + rlo) + 32 * g_c) ^ (s_c + 8 * g_c)) * 16));
 
   uint32_t oa[16], ob[4], osb[4];
-  v4i ga[8];            // one staging batch
+  v4i ga[8];            // two staging quarters (register sets 0 and 1)
   v4i bc[2][4][2];      // weight codes [chunk parity][panel][half]
   uint32_t bs[2][4];    // weight E4M3 scales [chunk parity][panel]
   float sw[4][4];       // weight block scales of the current chunk, fp32 [panel][block]
@@ -2276,15 +2277,18 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
   v16f acc[4][4];
 
   auto kcl = [&](int kc) __attribute__((always_inline)) { return kc < kcn ? kc : kcn - 1; };
-  auto load_a = [&](int kc, int b) __attribute__((always_inline)) {
+  // quarter q of the thread's 16 pieces (rows 16 i + tid / 16, i = 4 q ..
+  // 4 q + 3) through register set q % 2
+  auto load_a = [&](int kc, int q) __attribute__((always_inline)) {
 #pragma unroll
-    for (int it = 0; it < 8; ++it) ga[it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[8 * b + it], kcl(kc) * 256, 0);
+    for (int it = 0; it < 4; ++it)
+      ga[4 * (q & 1) + it] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[4 * q + it], kcl(kc) * 256, 0);
   };
-  auto write_a = [&](uint8_t* st, int b, int from, int to) __attribute__((always_inline)) {
+  auto write_a = [&](uint8_t* st, int q) __attribute__((always_inline)) {
 #pragma unroll
-    for (int it = 0; it < 8; ++it) {
-      const int i = 8 * b + it;
-      if (it >= from && it < to) *reinterpret_cast<v4i*>(st + (i >> 1) * 8192 + la_pair[i & 1]) = ga[it];
+    for (int it = 0; it < 4; ++it) {
+      const int i = 4 * q + it;
+      *reinterpret_cast<v4i*>(st + (i >> 1) * 8192 + la_pair[i & 1]) = ga[4 * (q & 1) + it];
     }
   };
   auto load_b = [&](auto Pc, int kc) __attribute__((always_inline)) {
@@ -2334,7 +2338,7 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
       if (t < nvmem) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       if (t < nds_r) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (t < nds_w) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
@@ -2348,17 +2352,21 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
     constexpr std::integral_constant<int, P ^ 1> Q{};
 #pragma unroll
     for (int s = 0; s < 7; ++s) {
-      // step 0: weights of chunk kc + 1 and the first activation batch of
-      // kc + 1; step 3: that batch into LDS, the second batch loaded; step 6:
-      // the second batch into LDS
-      if (s == 0) { load_b(Q, kc + 1); load_a(kc + 1, 0); }
-      if (s == 3) { write_a(nxt, 0, 0, 8); load_a(kc + 1, 1); }
-      if (s == 5) write_a(nxt, 1, 0, 4);
-      if (s == 6) write_a(nxt, 1, 4, 8);
+      // the activations of chunk kc + 1 in quarters of four pieces through
+      // two register sets: quarters 0 and 1 loaded in step 0, stored in steps
+      // 2 and 3, where quarters 2 and 3 are loaded into the freed sets and
+      // stored in steps 5 and 6 (two or three steps for each load); at most
+      // four stores and four loads per step keep the compiler on the
+      // MFMA / expansion interleave
+      if (s == 0) { load_b(Q, kc + 1); load_a(kc + 1, 0); load_a(kc + 1, 1); }
+      if (s == 2) { write_a(nxt, 0); load_a(kc + 1, 2); }
+      if (s == 3) { write_a(nxt, 1); load_a(kc + 1, 3); }
+      if (s == 5) write_a(nxt, 2);
+      if (s == 6) write_a(nxt, 3);
       read_a(cur, s + 1, (s + 1) & 1);
       mfmas(s & 1);
       expand(Pc, s + 1, (s + 1) & 1);
-      interleave(s == 0 ? 20 : s == 3 ? 8 : 0, 4, (s == 3) ? 8 : (s >= 5) ? 4 : 0);
+      interleave(s == 0 ? 20 : (s == 2 || s == 3) ? 4 : 0, 4, (s == 2 || s == 3 || s >= 5) ? 4 : 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
@@ -2399,10 +2407,11 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
     int kc = 0;
     if (kcn & 1) {
       load_b(std::integral_constant<int, 0>(), 0);
-      load_a(0, 0);
-      write_a(smem, 0, 0, 8);
-      load_a(0, 1);
-      write_a(smem, 1, 0, 8);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        load_a(0, q);
+        write_a(smem, q);
+      }
       __syncthreads();
       convert_b_scales(std::integral_constant<int, 0>());
 #pragma unroll
@@ -2416,10 +2425,11 @@ __global__ void __launch_bounds__(256) k_gemm_w4a16_direct(GemmArgs g) {
     }
     if (kc < kcn) {
       load_b(std::integral_constant<int, 0>(), kc);
-      load_a(kc, 0);
-      write_a(smem, 0, 0, 8);
-      load_a(kc, 1);
-      write_a(smem, 1, 0, 8);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        load_a(kc, q);
+        write_a(smem, q);
+      }
       __syncthreads();
       read_a(smem, 0, 0);
       convert_b_scales(std::integral_constant<int, 0>());

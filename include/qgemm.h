@@ -108,7 +108,8 @@ typedef enum qg_out_dtype {
  *                 E8M0 bytes; must be NULL for FP8.
  *   tensor_scale  out: one fp32 decode scale; must be NULL for the MX formats.
  *   A tensor of at most 3072 units of 16 elements (units per row:
- *   ceil(cols / 16)) is quantized by one single-workgroup kernel. For a
+ *   ceil(cols / 16)) is quantized by one launch, whose workgroups each
+ *   reduce the whole tensor and code their share of it. For a
  *   larger one the tensor-wide max is reduced in two kernels whose partial
  *   results are parked in `codes` (overwritten by the codes afterwards), then
  *   a third codes the elements. Either way x, codes, block_scales and

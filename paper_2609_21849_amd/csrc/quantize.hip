@@ -279,10 +279,11 @@ __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict_
 
 // ---------------------------------------------------------------- small tensors
 // The whole dynamic quantization of a small tensor (at most 3072 units of 16
-// elements) in one workgroup: every thread loads its (up to three) units into
-// registers at once, the workgroup reduces the max, and the codes come from
-// the same registers -- one launch and one read instead of the three-kernel
-// chain, whose launch latencies dominate at these sizes. The same arithmetic
+// elements) in one launch: every workgroup loads the whole tensor into
+// registers (up to three units per thread) and reduces its max; workgroup b
+// of G codes its G-th of the units from the same registers -- one launch
+// instead of the three-kernel chain, whose launch latencies dominate at these
+// sizes, with the coding and the stores spread over G CUs. The same arithmetic
 // as the chain, so the same bits: the max of the bf16 magnitude bits,
 // s = fl(amax / 448) or fl(amax / 2688) (NaN if the tensor holds inf or NaN),
 // then the unit helpers above. FP8 rows may end in a shorter unit; NVFP4
@@ -290,21 +291,23 @@ __global__ void __launch_bounds__(256) k_quant_nvfp4(const uint16_t* __restrict_
 // elements; vec_store (FP8): 16-byte aligned codes and cols % 16 == 0.
 constexpr int kSmallPerThread = 3;
 constexpr int64_t kSmallUnits = 1024 * kSmallPerThread;
+constexpr int64_t kSmallGroups = 8;  // workgroups that share the coding
 
 template <int FMT, bool VEC>
 __global__ void __launch_bounds__(1024) k_quant_small(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
                                                       int64_t ldx, uint8_t* __restrict__ q,
                                                       uint8_t* __restrict__ bscale, float* __restrict__ tscale,
                                                       bool vec_store) {
-  const int64_t upr = (cols + 15) >> 4;
-  const int64_t units = rows * upr;
+  // at most kSmallUnits units: 32-bit unit arithmetic
+  const int upr = (int)((cols + 15) >> 4);
+  const int units = (int)rows * upr;
   uint32_t w[kSmallPerThread][8];
 #pragma unroll
   for (int i = 0; i < kSmallPerThread; ++i) {
-    const int64_t u = threadIdx.x + 1024 * i;
+    const int u = (int)threadIdx.x + 1024 * i;
     if (u < units) {
-      const int64_t row = u / upr, c = (u - row * upr) * 16;
-      unit_load<VEC>(x + row * ldx + c, min((int64_t)16, cols - c), w[i]);
+      const int row = u / upr, c = (u - row * upr) * 16;
+      unit_load<VEC>(x + (int64_t)row * ldx + c, min((int64_t)16, cols - c), w[i]);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) w[i][j] = 0u;
@@ -327,15 +330,19 @@ __global__ void __launch_bounds__(1024) k_quant_small(const uint16_t* __restrict
   for (int i = 0; i < 16; ++i) a = max(a, part[i]);
   a <<= 16;
   const float s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), FMT == 1 ? 448.0f : 2688.0f);
-  if (threadIdx.x == 0) *tscale = s;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *tscale = s;
+  // every workgroup reduces the whole tensor; workgroup b codes the units
+  // [b U / G, (b + 1) U / G) of the U units (G workgroups)
+  const int lo = gridDim.x == 1 ? 0 : units * (int)blockIdx.x / (int)gridDim.x;
+  const int hi = gridDim.x == 1 ? units : units * ((int)blockIdx.x + 1) / (int)gridDim.x;
   const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
 #pragma unroll
   for (int i = 0; i < kSmallPerThread; ++i) {
-    const int64_t u = threadIdx.x + 1024 * i;
-    if (u >= units) continue;
-    const int64_t row = u / upr, c = (u - row * upr) * 16;
-    if (FMT == 1) quant_fp8_words(w[i], min((int64_t)16, cols - c), q + row * cols + c, r, vec_store);
-    else bscale[u] = (uint8_t)quant_nvfp4_words(w[i], q + u * 8, s);
+    const int u = (int)threadIdx.x + 1024 * i;
+    if (u < lo || u >= hi) continue;
+    const int row = u / upr, c = (u - row * upr) * 16;
+    if (FMT == 1) quant_fp8_words(w[i], min((int64_t)16, cols - c), q + (int64_t)row * cols + c, r, vec_store);
+    else bscale[u] = (uint8_t)quant_nvfp4_words(w[i], q + (int64_t)u * 8, s);
   }
 }
 
@@ -650,19 +657,23 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
   const bool contig = (ldx == cols);
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0);
   if (rows * ((cols + 15) / 16) <= kSmallUnits) {
-    // one workgroup does it all (NVFP4 codes are 8-byte aligned: checked by
-    // the caller). Measured against the chain (GPU time from graph replays):
-    // 1 x 1024 .. 3072 3.4 against 6.2-6.7 us, 128 x 256 5.2 against
-    // 6.5-7.3 us, 16 x 3072 6.2-6.6 against 6.5-7.4 us; at 4096 units
-    // (64 Ki elements) the two were level.
+    // one launch does it all (NVFP4 codes are 8-byte aligned: checked by
+    // the caller); one workgroup per 256 units, at most eight. Measured
+    // against the chain (GPU time from graph replays): 1 x 1024 3.1 us,
+    // 128 x 256 4.3 us, 16 x 3072 4.6 us, where the chain takes 6.5 us
+    // (FP8) to 7.4 us (NVFP4); one workgroup took 5.0 and 5.9 us on the last
+    // two. Raising the limit to 8192 units (eight per thread) lost to the
+    // chain from 6144 units on.
     const bool rvec = aligned && (cols % 8 == 0) && (contig || ldx % 8 == 0);
     const bool qvec = (reinterpret_cast<uintptr_t>(codes) % 16 == 0) && (cols % 16 == 0);
+    const int64_t units = rows * ((cols + 15) / 16);
+    const unsigned G = (unsigned)std::min<int64_t>(kSmallGroups, (units + 255) / 256);
     if (fmt == 1) {
-      if (rvec) hipLaunchKernelGGL((k_quant_small<1, true>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
-      else hipLaunchKernelGGL((k_quant_small<1, false>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
+      if (rvec) hipLaunchKernelGGL((k_quant_small<1, true>), dim3(G), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
+      else hipLaunchKernelGGL((k_quant_small<1, false>), dim3(G), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, qvec);
     } else {
-      if (rvec) hipLaunchKernelGGL((k_quant_small<2, true>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
-      else hipLaunchKernelGGL((k_quant_small<2, false>), dim3(1), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
+      if (rvec) hipLaunchKernelGGL((k_quant_small<2, true>), dim3(G), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
+      else hipLaunchKernelGGL((k_quant_small<2, false>), dim3(G), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
     }
     return hipGetLastError();
   }

@@ -144,10 +144,12 @@ def test_tiny_blocks_get_subnormal_scales():
 
 
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
-@pytest.mark.parametrize("rows,cols,bad", [(4, 64, 0x7F80), (600, 1024, 0x7F80), (600, 1024, 0xFFC1)])
+@pytest.mark.parametrize("rows,cols,bad", [(4, 64, 0x7F80), (16, 3072, 0xFFC1), (600, 1024, 0x7F80),
+                                            (600, 1024, 0xFFC1)])
 def test_nonfinite_input_gives_nan_scale(fmt, rows, cols, bad):
-    # +inf or a NaN anywhere: the single-workgroup kernel (4 x 64) and the
-    # three-kernel chain (600 x 1024) both leave a NaN tensor scale
+    # +inf or a NaN anywhere: the single-launch small-tensor kernel (one
+    # workgroup at 4 x 64, eight at 16 x 3072) and the three-kernel chain
+    # (600 x 1024) all leave a NaN tensor scale
     x = synth.normal_bf16(rows, cols, 1.0, 7, 0)
     x[rows // 2, 9] = bad
     qt = q.quantize(to_dev_bf16(x), fmt)

@@ -109,11 +109,14 @@ typedef enum qg_out_dtype {
  *   tensor_scale  out: one fp32 decode scale; must be NULL for the MX formats.
  *   A tensor of at most 3072 units of 16 elements (units per row:
  *   ceil(cols / 16)) is quantized by one launch, whose workgroups each
- *   reduce the whole tensor and code their share of it. For a
- *   larger one the tensor-wide max is reduced in two kernels whose partial
- *   results are parked in `codes` (overwritten by the codes afterwards), then
- *   a third codes the elements. Either way x, codes, block_scales and
- *   tensor_scale must not overlap.
+ *   reduce the whole tensor and code their share of it. A dense one
+ *   (ldx == cols, 16-byte aligned x, 8-byte aligned codes, rows * cols a
+ *   multiple of 8) of at most 3 Mi elements takes two launches: the first
+ *   leaves its partial maxima in `codes`, the second reduces them and writes
+ *   the codes over them. Any other tensor-wide max is reduced in two kernels
+ *   whose partial results are parked in `codes` the same way, then a third
+ *   codes the elements. Always x, codes, block_scales and tensor_scale must
+ *   not overlap.
  *
  * Arithmetic (bit-exact; every step one IEEE binary32 operation, RNE):
  *   FP8  : a = max|x|; s = a/448; r = s>0 ? 1/s : 0; q = E4M3(x*r)

@@ -7,9 +7,10 @@
 // paragraph; Table 2). The same kernels quantize weights offline (PTQ).
 //
 // A tensor-wide scale needs the tensor-wide max before any element can be
-// coded. A small tensor (at most 3072 units of 16 elements) is quantized by
-// one workgroup in one kernel (k_quant_small); any other is a short chain on
-// the caller's stream:
+// coded. A small tensor (at most 3072 units of 16 elements) is quantized in
+// one launch (k_quant_small); a dense one of at most 3 Mi elements in two
+// (k_amax_slots, k_quant_dense_slots: the maxima handed over inside the code
+// buffer); any other is a short chain on the caller's stream:
 //   k_amax_partial : max |x| as an integer max of bf16 magnitude bits (the
 //                    bit pattern of a non-negative value orders like the
 //                    value); one partial per workgroup, parked in the code
@@ -347,6 +348,47 @@ __global__ void __launch_bounds__(1024) k_quant_small(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------- dense tensors
+// Codes of one whole 16-byte unit (8 consecutive elements, index u) held in
+// `raw`: FP8 one 8-byte store, NVFP4 one 4-byte store plus, on the even lane
+// of a lane pair, the block scale (lanes 2j and 2j+1 hold the two halves of
+// one 16-element block and share its max with one lane swap, so every lane
+// of the wave must call this together; `in` only gates the stores).
+template <int FMT>
+__device__ inline void code_unit8(const uint4 raw, int64_t u, bool in, uint8_t* __restrict__ q,
+                                  uint8_t* __restrict__ bscale, float s, float r, float d_t, int lane) {
+  const uint32_t ww[4] = {raw.x, raw.y, raw.z, raw.w};
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = bf16_lo(ww[j]);
+    v[2 * j + 1] = bf16_hi(ww[j]);
+  }
+  if (FMT == 1) {
+    float y[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
+    const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
+    if (in) *reinterpret_cast<uint2*>(q + u * 8) = make_uint2(lo, hi);
+  } else {
+    uint32_t am = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
+    am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+    const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(am), d_t) : 0.0f;
+    const uint32_t sb = enc_e4m3(vb);
+    const float S = __fmul_rn(dec_e4m3(sb), s);
+    const float rb = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
+    float y[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], rb);
+    const uint32_t w = hw_e2m1x8(y);
+    if (in) {
+      *reinterpret_cast<uint32_t*>(q + u * 4) = w;
+      if ((lane & 1) == 0) bscale[u >> 1] = (uint8_t)sb;
+    }
+  }
+}
+
 // Dense tensors (ldx == cols, 16-byte aligned rows): each wavefront codes a
 // chunk of 512 H consecutive elements. Lane l reads elements
 // [512 h + 8l, 512 h + 8l + 8) of the chunk for h < H with one 16-byte load
@@ -376,45 +418,119 @@ __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict_
   for (int h = 0; h < H; ++h) {
     const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
     const bool full = (e0 + 8 <= n);
-    float v[8];
-    if (full) {
-      const uint32_t ww[4] = {raw[h].x, raw[h].y, raw[h].z, raw[h].w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v[2 * j] = bf16_lo(ww[j]);
-        v[2 * j + 1] = bf16_hi(ww[j]);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = (e0 + j < n) ? u2f((uint32_t)x[e0 + j] << 16) : 0.0f;
-    }
-    if (FMT == 1) {
+    code_unit8<FMT>(raw[h], e0 >> 3, full, q, bscale, s, r, d_t, lane);
+    if (FMT == 1 && !full && e0 < n) {  // FP8 tail unit of fewer than 8 elements
       float y[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
+      for (int j = 0; j < 8; ++j) y[j] = (e0 + j < n) ? __fmul_rn(u2f((uint32_t)x[e0 + j] << 16), r) : 0.0f;
       const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
-      if (full) {
-        *reinterpret_cast<uint2*>(q + e0) = make_uint2(lo, hi);
-      } else {
-        for (int j = 0; j < 8 && e0 + j < n; ++j) q[e0 + j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
-      }
-    } else {
-      uint32_t am = 0;
+      for (int j = 0; j < 8 && e0 + j < n; ++j) q[e0 + j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- dense, two launches
+// Dynamic quantization of a dense tensor without the one-workgroup finalize
+// kernel. k_amax_slots leaves each of its P workgroup maxima not in one
+// place but in every code region of the quantize launch (slot i among the
+// first 4 P bytes of each region); each workgroup of k_quant_dense_slots
+// reduces the P maxima found at the start of its own region to the tensor
+// scale before any of its codes overwrite them. No workgroup reads what
+// another writes within a launch, so stream order between the two launches
+// is the only synchronisation, and the caller's code buffer the only memory.
+// Region j of G: the 16-byte units [slot_region_lo(j), slot_region_lo(j + 1))
+// of the n / 8 (the last region ends at n / 8), whose codes start at byte CB
+// times their first unit (CB = 8 for FP8, 4 for NVFP4). The host picks G so
+// that every region's codes hold the 4 P bytes of slots.
+__device__ inline int64_t slot_region_lo(int64_t pairs, int64_t j, int64_t g) { return 2 * (pairs * j / g); }
+constexpr int kSlotsAmaxLoads = 4;          // 16-byte loads per lane in flight
+constexpr int64_t kSlotsAmaxGroups = 1024;  // P, a multiple of 8
+constexpr int64_t kSlotsQuantGroups = 2048;
+// The P x G scattered 4-byte slot stores grow with the tensor: at 4608 x
+// 3072 (P = 1024 or 512, G = 1728 or 1024) the two launches took 17-22 us
+// against the chain's 12.4 (GPU time from graph replays); at 256 x 3072 5.7
+// against 6.7 us (FP8) and 6.4 against 7.7 (NVFP4), at 512 x 3072 6.2 against
+// 7.0 and 6.8 against 7.9, level from 3 Mi elements on (1024 x 4096: 8.2
+// against 7.8). Larger tensors take the chain.
+constexpr int64_t kSlotsMaxElements = int64_t(3) << 20;
+
+template <int U>
+__global__ void __launch_bounds__(256) k_amax_slots(const uint16_t* __restrict__ x, int64_t units,
+                                                    uint8_t* __restrict__ q, int cb, int gq) {
+  const uint4* xv = reinterpret_cast<const uint4*>(x);
+  uint32_t m = 0;
+  for (int64_t base = (int64_t)blockIdx.x * 256 * U + threadIdx.x; base < units; base += (int64_t)gridDim.x * 256 * U) {
+    uint4 v[U];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
-      am = max(am, (uint32_t)__shfl_xor((int)am, 1));
-      const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(am), d_t) : 0.0f;
-      const uint32_t sb = enc_e4m3(vb);
-      const float S = __fmul_rn(dec_e4m3(sb), s);
-      const float rb = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
-      float y[8];
+    for (int u = 0; u < U; ++u) v[u] = (base + u * 256 < units) ? xv[base + u * 256] : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], rb);
-      const uint32_t w = hw_e2m1x8(y);
-      if (full) {
-        *reinterpret_cast<uint32_t*>(q + (e0 >> 1)) = w;
-        if ((lane & 1) == 0) bscale[e0 >> 4] = (uint8_t)sb;
+    for (int u = 0; u < U; ++u) {
+      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t t = w[i] & 0x7FFF7FFFu;
+        m = max(m, max(t & 0xFFFFu, t >> 16));
       }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  const uint32_t mw = max(max(part[0], part[1]), max(part[2], part[3]));
+  // workgroup b runs on XCD b mod 8: with the slots ordered XCD-major, the
+  // maxima of one XCD's workgroups fill whole cache lines of each region
+  const int P = (int)gridDim.x, b = (int)blockIdx.x;
+  const int slot = (P % 8 == 0) ? (b % 8) * (P / 8) + b / 8 : b;
+  const int64_t pairs = units >> 1;
+  for (int j = (int)threadIdx.x; j < gq; j += 256)
+    reinterpret_cast<uint32_t*>(q + slot_region_lo(pairs, j, gq) * cb)[slot] = mw;
+}
+
+// Each wave codes runs of 64 consecutive units (one 16-byte load per lane,
+// four per lane in flight); rounds of 1024 units until the region ends.
+template <int FMT>
+__global__ void __launch_bounds__(256) k_quant_dense_slots(const uint16_t* __restrict__ x, int64_t units,
+                                                           uint8_t* __restrict__ q, uint8_t* __restrict__ bscale,
+                                                           float* __restrict__ tscale, int P) {
+  constexpr int H = 4;
+  constexpr int CB = FMT == 1 ? 8 : 4;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t pairs = units >> 1;
+  const int64_t lo = slot_region_lo(pairs, blockIdx.x, gridDim.x);
+  const int64_t hi = (blockIdx.x + 1 == gridDim.x) ? units : slot_region_lo(pairs, blockIdx.x + 1, gridDim.x);
+  const uint4* xv = reinterpret_cast<const uint4*>(x);
+  uint4 raw[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const int64_t u = lo + 256 * wv + 64 * h + lane;
+    raw[h] = (u < hi) ? xv[u] : make_uint4(0u, 0u, 0u, 0u);
+  }
+  // the tensor max from this region's slots, all read before the barrier
+  const uint32_t* slots = reinterpret_cast<const uint32_t*>(q + lo * CB);
+  uint32_t m = 0;
+  for (int i = (int)threadIdx.x; i < P; i += 256) m = max(m, slots[i]);
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t part[4];
+  if (lane == 0) part[wv] = m;
+  __syncthreads();
+  const uint32_t a = max(max(part[0], part[1]), max(part[2], part[3])) << 16;
+  const float s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), FMT == 1 ? 448.0f : 2688.0f);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *tscale = s;
+  const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
+  const float d_t = __fmul_rn(6.0f, s);
+  for (int64_t base = lo;;) {
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const int64_t u = base + 256 * wv + 64 * h + lane;
+      code_unit8<FMT>(raw[h], u, u < hi, q, bscale, s, r, d_t, lane);
+    }
+    base += 1024;
+    if (base >= hi) break;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const int64_t u = base + 256 * wv + 64 * h + lane;
+      raw[h] = (u < hi) ? xv[u] : make_uint4(0u, 0u, 0u, 0u);
     }
   }
 }
@@ -676,6 +792,23 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
       else hipLaunchKernelGGL((k_quant_small<2, false>), dim3(G), dim3(1024), 0, st, x, rows, cols, ldx, codes, bscale, tscale, false);
     }
     return hipGetLastError();
+  }
+  const int64_t n = rows * cols;
+  if (contig && aligned && n % 8 == 0 && n <= kSlotsMaxElements && reinterpret_cast<uintptr_t>(codes) % 8 == 0) {
+    // dense: two launches, the maxima handed over in every code region
+    const int64_t units = n / 8, pairs = units / 2;
+    const int cb = (fmt == 1) ? 8 : 4;
+    const int64_t P = std::min<int64_t>(kSlotsAmaxGroups, ((units + 256 * kSlotsAmaxLoads - 1) / (256 * kSlotsAmaxLoads) + 7) / 8 * 8);
+    const int64_t need = (4 * P + 2 * cb - 1) / (2 * cb);  // unit pairs per region that hold the slots
+    const int64_t G = std::min<int64_t>(std::min<int64_t>(kSlotsQuantGroups, (units + 1023) / 1024), pairs / need);
+    if (G >= 1) {
+      hipLaunchKernelGGL(k_amax_slots<kSlotsAmaxLoads>, dim3((unsigned)P), dim3(256), 0, st, x, units, codes, cb, (int)G);
+      if (fmt == 1)
+        hipLaunchKernelGGL(k_quant_dense_slots<1>, dim3((unsigned)G), dim3(256), 0, st, x, units, codes, bscale, tscale, (int)P);
+      else
+        hipLaunchKernelGGL(k_quant_dense_slots<2>, dim3((unsigned)G), dim3(256), 0, st, x, units, codes, bscale, tscale, (int)P);
+      return hipGetLastError();
+    }
   }
   // amax: per-workgroup partial maxima are parked in the code buffer, which
   // the quantize kernel overwrites afterwards (stream order separates them).

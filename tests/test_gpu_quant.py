@@ -81,6 +81,45 @@ def test_strided_rows_past_the_small_limit(fmt, offset):
     assert_quant_equal(qt, np.ascontiguousarray(full[:, offset:offset + 1024]))
 
 
+@pytest.mark.parametrize("fmt,rows,cols", [(FP8, 3073, 16), (NVFP4, 3073, 16), (FP8, 1001, 1000),
+                                           (FP8, 600, 1024), (NVFP4, 600, 1024), (FP8, 512, 3072),
+                                           (NVFP4, 512, 3072), (FP8, 1024, 3072), (NVFP4, 1025, 3072)])
+@pytest.mark.parametrize("where", ["first", "last"])
+def test_dense_two_launch_path(fmt, rows, cols, where):
+    # dense tensors past the small limit: the amax launch hands its maxima to
+    # every code region of the quantize launch (3073 x 16: 3073 units, just
+    # past the small kernel; 1001 x 1000: an odd number of 8-element units;
+    # 1024 x 3072: the largest such tensor, 1025 x 3072 the chain); the
+    # tensor max sits in the first or the last region
+    x = synth.normal_bf16(rows, cols, 1.0, 11, 0, outlier_frac=0.001, outlier_gain=20.0)
+    if where == "first":
+        x[0, 1] = 0xC300   # -128
+    else:
+        x[rows - 1, cols - 1] = 0x4300   # 128
+    qt = q.quantize(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, x)
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_dense_two_launch_zero_and_reuse(fmt):
+    # an all-zero dense tensor (scale 0, every code 0), then a tensor with a
+    # much smaller max quantized into the same buffers, which hold the first
+    # call's codes: every handed-over maximum must be the second call's
+    rows, cols = 600, 1024
+    z = np.zeros((rows, cols), np.uint16)
+    qt = q.quantize(to_dev_bf16(z), fmt)
+    torch.cuda.synchronize()
+    assert_quant_equal(qt, z)
+    big = synth.normal_bf16(rows, cols, 100.0, 12, 0)
+    small = synth.normal_bf16(rows, cols, 0.01, 13, 0)
+    for x in (big, small):
+        xd = to_dev_bf16(x)
+        q.qg_quantize_act(fmt, xd, rows, cols, cols, qt.codes, qt.block_scales, qt.tensor_scale)
+        torch.cuda.synchronize()
+        assert_quant_equal(qt, x)
+
+
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
 def test_row_stride_larger_than_row(fmt):
     full = synth.normal_bf16(64, 400, 1.0, 4, 0)
@@ -148,8 +187,8 @@ def test_tiny_blocks_get_subnormal_scales():
                                             (600, 1024, 0xFFC1)])
 def test_nonfinite_input_gives_nan_scale(fmt, rows, cols, bad):
     # +inf or a NaN anywhere: the single-launch small-tensor kernel (one
-    # workgroup at 4 x 64, eight at 16 x 3072) and the three-kernel chain
-    # (600 x 1024) all leave a NaN tensor scale
+    # workgroup at 4 x 64, eight at 16 x 3072) and the two-launch dense path
+    # (600 x 1024) both leave a NaN tensor scale
     x = synth.normal_bf16(rows, cols, 1.0, 7, 0)
     x[rows // 2, 9] = bad
     qt = q.quantize(to_dev_bf16(x), fmt)

@@ -121,6 +121,26 @@ def test_dense_two_launch_zero_and_reuse(fmt):
 
 
 @pytest.mark.parametrize("fmt", [FP8, NVFP4])
+def test_concurrent_calls_on_two_streams(fmt):
+    # the dynamic quantizers keep no state of their own (their partial maxima
+    # live in each call's code buffer), so calls on two streams may overlap:
+    # a dense tensor on the two-launch path and one on the three-kernel chain,
+    # each issued several times on its own stream
+    xa = synth.normal_bf16(600, 1024, 1.0, 14, 0, outlier_frac=0.001, outlier_gain=50.0)
+    xb = synth.normal_bf16(2048, 3072, 0.5, 15, 0, outlier_frac=0.001, outlier_gain=50.0)
+    da, db = to_dev_bf16(xa), to_dev_bf16(xb)
+    qa, qb = q.quantize(da, fmt), q.quantize(db, fmt)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(4):
+        q.qg_quantize_act(fmt, da, 600, 1024, 1024, qa.codes, qa.block_scales, qa.tensor_scale, stream=sa)
+        q.qg_quantize_act(fmt, db, 2048, 3072, 3072, qb.codes, qb.block_scales, qb.tensor_scale, stream=sb)
+    torch.cuda.synchronize()
+    assert_quant_equal(qa, xa)
+    assert_quant_equal(qb, xb)
+
+
+@pytest.mark.parametrize("fmt", [FP8, NVFP4])
 def test_row_stride_larger_than_row(fmt):
     full = synth.normal_bf16(64, 400, 1.0, 4, 0)
     xd = to_dev_bf16(full)[:, :320]

@@ -567,7 +567,8 @@ def main():
         "w4a16_pool_m16_gbs": pool["m16"]["gbs"], "w4a16_pool_m16_frac_of_hbm": pool["m16"]["frac_of_hbm_peak"],
         "w4a16_pool_m256_frac_of_bf16_peak": pool["m256"]["frac_of_bf16_peak"],
         "w4a16_pool_m512_frac_of_bf16_peak": pool["m512"]["frac_of_bf16_peak"],
-        "c1_fp8_128x256x256_linear_us": sl["c1_fp8_128x256x256"]["linear_us"],
+        "c1_fp8_128x256x256_linear_us": sl["c1_fp8_128x256x256"]["fused_linear_us"],
+        "c1_fp8_128x256x256_quantize_then_gemm_us": sl["c1_fp8_128x256x256"]["linear_us"],
         "c2_nvfp4_512x3072x3072_gemm_us": sl["c2_nvfp4_512x3072x3072"]["gemm_us"],
         "c2_nvfp4_frac_of_roofline_f16_mfma": sl["c2_nvfp4_512x3072x3072"]["frac_of_roofline_f16_mfma"],
     }
@@ -671,6 +672,21 @@ def single_linear_part(q, synth, reps=50):
         ent = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2), "linear_us": round(qus + gus, 2),
                "with_host_launch": {"quant_us": round(qus_l, 2), "gemm_us": round(gus_l, 2)},
                "gemm_tflops": round(flops / (gus * 1e6), 1), "gemm_algorithmic_mb": round(gbytes / 1e6, 2)}
+        if not nv:
+            # the same linear in one launch: qg_linear_fp8 quantizes the bf16
+            # activation inside the GEMM (same codes, scale and output bits)
+            largs = (x.data_ptr(), k, ts.data_ptr(), packed.data_ptr(), packed.numel(), m, n, k, y.data_ptr(), n,
+                     q.QG_OUT_BF16, st)
+            fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps + 5)]
+            for i in range(reps + 5):
+                fev[i][0].record()
+                assert lib.qg_linear_fp8(*largs) == 0
+                fev[i][1].record()
+            torch.cuda.synchronize()
+            fus_l = float(np.median([ev[0].elapsed_time(ev[1]) for ev in fev[5:]])) * 1e3
+            fus = graph_us(lambda s: lib.qg_linear_fp8(*largs[:-1], s)) or fus_l
+            ent["fused_linear_us"] = round(fus, 2)
+            ent["with_host_launch"]["fused_linear_us"] = round(fus_l, 2)
         if nv:
             t_f16 = max(flops / (PEAK["f16"] * 1e12), gbytes / (PEAK["hbm_gbs"] * 1e9)) * 1e6
             t_fp4 = max(flops / (PEAK["fp4"] * 1e12), gbytes / (PEAK["hbm_gbs"] * 1e9)) * 1e6
@@ -712,9 +728,15 @@ def w8a8_encoder_part(q, enc, reps=20):
         gus_l = float(np.mean([ev[1].elapsed_time(ev[2]) for ev in evs[3:]])) * 1e3
         qus = graph_us(lambda s: lib.qg_quantize_act(*qargs[:-1], s)) or qus_l
         gus = graph_us(lambda s: lib.qg_gemm(*gargs[:-1], s)) or gus_l
-        out["%s_m%d" % (e["name"], m)] = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2),
-                                            "gemm_tflops": round(2 * m * n * k / (gus * 1e6), 2),
-                                            "with_host_launch": {"quant_us": round(qus_l, 2), "gemm_us": round(gus_l, 2)}}
+        ent = {"quant_us": round(qus, 2), "gemm_us": round(gus, 2),
+               "gemm_tflops": round(2 * m * n * k / (gus * 1e6), 2),
+               "with_host_launch": {"quant_us": round(qus_l, 2), "gemm_us": round(gus_l, 2)}}
+        if m * k <= 65536:
+            # quantize + GEMM in one launch (qg_linear_fp8), same output bits
+            largs = (e["x"].data_ptr(), k, ts.data_ptr(), e["w8"].data_ptr(), e["w8"].numel(), m, n, k,
+                     y.data_ptr(), n, q.QG_OUT_BF16)
+            ent["fused_linear_us"] = round(graph_us(lambda s: lib.qg_linear_fp8(*largs, s)) or 0.0, 2)
+        out["%s_m%d" % (e["name"], m)] = ent
     return out
 
 

@@ -242,6 +242,34 @@ qg_status qg_gemm(qg_format a_fmt, const void *a, const void *a_block_scales,
                   void *y, int64_t ldy, qg_out_dtype y_dtype, void *stream);
 
 /*
+ * qg_linear_fp8 -- W8A8 linear layer straight from bf16 activations: the
+ * dynamic per-tensor FP8 quantization of qg_quantize_act done inside the
+ * GEMM of qg_gemm, one launch instead of two, for activations small enough
+ * that every workgroup reduces the whole tensor's max itself (few tokens:
+ * the single FP8 linear, the small encoder's linears). Paper: Sec. 4,
+ * quantization paragraph (activations quantized at run time for the FP8
+ * linears; the encoder runs on few tokens).
+ *   x               bf16 [m, ldx] activations, 16-byte aligned, ldx % 8 == 0,
+ *                   ldx >= k; not modified.
+ *   a_tensor_scale  out: device fp32, the decode scale s = fl(max|x| / 448)
+ *                   (NaN when x holds inf or NaN, 0 for an empty x), the bits
+ *                   qg_quantize_act writes for the same x.
+ *   w_packed        an FP8 weight [n, k] as written by qg_pack_weights.
+ *   y               out: [m, ldy] of y_dtype (bf16 or fp32).
+ * Result: the activation codes are those of qg_quantize_act; y is the value
+ * qg_gemm(FP8, FP8) returns for them, bit for bit where qg_gemm takes its
+ * few-token (split-K) kernel, which is every shape with m <= 1024 and at
+ * most two 32 x 64 tiles per compute unit; elsewhere within qg_gemm's
+ * accuracy contract. Shapes: n % 16 == 0, k % 128 == 0, ldy >= n and
+ * m * k <= 65536, else QG_ERR_SHAPE (a larger activation takes
+ * qg_quantize_act and qg_gemm). x, a_tensor_scale and y must not overlap.
+ */
+qg_status qg_linear_fp8(const void *x, int64_t ldx, float *a_tensor_scale,
+                        const void *w_packed, size_t w_packed_bytes,
+                        int64_t m, int64_t n, int64_t k,
+                        void *y, int64_t ldy, qg_out_dtype y_dtype, void *stream);
+
+/*
  * qg_gemm_quant -- qg_gemm whose epilogue writes the output already
  * quantized to FP8 E4M3 with a static (calibrated) decode scale: the next
  * linear's activation operand, produced without the bf16 round trip through

@@ -25,6 +25,7 @@ QG_OK = 0
 STATUS_NAMES = {0: "QG_OK", 1: "QG_ERR_INVALID_ARG", 2: "QG_ERR_UNSUPPORTED", 3: "QG_ERR_SHAPE",
                 4: "QG_ERR_BUFFER_TOO_SMALL", 5: "QG_ERR_HIP"}
 EXPORTS = ["qg_quantize_act", "qg_quantize_act_static", "qg_packed_bytes", "qg_pack_weights", "qg_unpack_weights", "qg_gemm",
+           "qg_linear_fp8",
            "qg_gemm_quant", "qg_gemm_quant_nvfp4", "qg_dequant", "qg_run_layers", "qg_stream_simulate", "qg_stream_plan", "qg_status_string",
            "qg_last_hip_error", "qg_abi_version"]
 
@@ -68,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.qg_unpack_weights.argtypes = [I32, P, SZ, I64, I64, P, P, P, P]
         L.qg_gemm.restype = I32
         L.qg_gemm.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, I32, P]
+        L.qg_linear_fp8.restype = I32
+        L.qg_linear_fp8.argtypes = [P, I64, P, P, SZ, I64, I64, I64, P, I64, I32, P]
         L.qg_gemm_quant.restype = I32
         L.qg_gemm_quant.argtypes = [I32, P, P, P, I64, I32, P, SZ, I64, I64, I64, P, I64, P, P]
         L.qg_gemm_quant_nvfp4.restype = I32
@@ -205,6 +208,15 @@ def qg_gemm(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_pa
     return s
 
 
+def qg_linear_fp8(x, ldx, a_tensor_scale, w_packed, w_packed_bytes, m, n, k, y, ldy, y_dtype, stream=None,
+                  check=True):
+    s = lib().qg_linear_fp8(_p(x), ldx, _p(a_tensor_scale), _p(w_packed), w_packed_bytes, m, n, k, _p(y), ldy,
+                            y_dtype, _stream(stream))
+    if check:
+        _check(s, "qg_linear_fp8")
+    return s
+
+
 def qg_gemm_quant(a_fmt, a, a_block_scales, a_tensor_scale, lda, w_fmt, w_packed, w_packed_bytes, m, n, k,
                   y_codes, ldy, y_scale, stream=None, check=True):
     s = lib().qg_gemm_quant(a_fmt, _p(a), _p(a_block_scales), _p(a_tensor_scale), lda, w_fmt, _p(w_packed),
@@ -236,6 +248,21 @@ def linear_nvfp4_out(a, w_packed, w_fmt: int, n: int, y_tensor_scale, stream=Non
     qg_gemm_quant_nvfp4(a_fmt, a_data, a_bs, a_ts, lda, w_fmt, w_packed, w_packed.numel(), m, n, k, codes, bs, n,
                         y_tensor_scale, stream)
     return QTensor(QG_FMT_NVFP4, codes, bs, y_tensor_scale, m, n)
+
+
+def linear_fp8(x, w_packed, n: int, out_dtype: int = QG_OUT_BF16, stream=None):
+    """Y = Q(x) . W^T from a bf16 activation x [m, k] (rows 16-byte aligned):
+    the FP8 activation quantization inside the GEMM. Returns (y, the
+    activation's decode scale as a one-element fp32 tensor)."""
+    import torch
+    _need(x, "x", torch.bfloat16, dense=False)
+    _need(w_packed, "w_packed", torch.uint8, None, x.device)
+    m, k = x.shape
+    ts = torch.empty(1, dtype=torch.float32, device=x.device)
+    y = torch.empty((m, n), dtype=torch.float32 if out_dtype == QG_OUT_F32 else torch.bfloat16, device=x.device)
+    ldx = x.stride(0) if m > 1 else k
+    qg_linear_fp8(x, ldx, ts, w_packed, w_packed.numel(), m, n, k, y, n, out_dtype, stream)
+    return y, ts
 
 
 def linear_fp8_out(a, w_packed, w_fmt: int, n: int, y_scale, stream=None) -> "QTensor":

@@ -38,6 +38,8 @@ bool is_mx(int f) { return f == QG_FMT_MXFP4 || f == QG_FMT_MXFP8; }
 uintptr_t mx_code_align(int f) { return f == QG_FMT_MXFP4 ? 4 : 8; }
 
 constexpr int64_t kMaxDim = std::numeric_limits<int32_t>::max();
+// qg_linear_fp8: every workgroup reduces the whole activation's max itself
+constexpr int64_t kLinearFp8MaxElements = 65536;
 
 }  // namespace
 
@@ -275,6 +277,34 @@ qg_status qg_gemm(qg_format a_fmt, const void* a, const void* a_block_scales,
     qg::log_call("qg_gemm", st_, "a_fmt=%d w_fmt=%d m=%lld n=%lld k=%lld lda=%lld ldy=%lld y_dtype=%d",
                  (int)a_fmt, (int)w_fmt, (long long)m, (long long)n, (long long)k, (long long)lda,
                  (long long)ldy, (int)y_dtype);
+  return st_;
+}
+
+qg_status qg_linear_fp8(const void* x, int64_t ldx, float* a_tensor_scale, const void* w_packed,
+                        size_t w_packed_bytes, int64_t m, int64_t n, int64_t k, void* y, int64_t ldy,
+                        qg_out_dtype y_dtype, void* stream) {
+  const qg_status st_ = [&]() -> qg_status {
+    if (y_dtype != QG_OUT_BF16 && y_dtype != QG_OUT_F32) return QG_ERR_INVALID_ARG;
+    if (a_tensor_scale == nullptr || !aligned(a_tensor_scale, 4)) return QG_ERR_INVALID_ARG;
+    if (m < 0 || n < 0 || k < 0 || m > kMaxDim || n > kMaxDim || k > kMaxDim) return QG_ERR_INVALID_ARG;
+    if (n % 16 != 0 || k % 128 != 0) return QG_ERR_SHAPE;
+    if (m * k > kLinearFp8MaxElements) return QG_ERR_SHAPE;
+    if (m > 0 && (ldx < k || ldy < n)) return QG_ERR_INVALID_ARG;
+    if (w_packed == nullptr || !aligned(w_packed, 256)) return QG_ERR_INVALID_ARG;
+    if (w_packed_bytes < (size_t)qg::packed_total_bytes(QG_FMT_FP8_E4M3, n, k)) return QG_ERR_BUFFER_TOO_SMALL;
+    if (qg::packed_total_bytes(QG_FMT_FP8_E4M3, n, k) > kMaxDim) return QG_ERR_SHAPE;
+    if (m > 0 && k > 0) {
+      if (x == nullptr || !aligned(x, 16) || ldx % 8 != 0) return QG_ERR_INVALID_ARG;
+      if (((m - 1) * ldx + k) * 2 > kMaxDim) return QG_ERR_SHAPE;
+    }
+    if (m > 0 && n > 0 && (y == nullptr || !aligned(y, y_dtype == QG_OUT_F32 ? 4 : 2))) return QG_ERR_INVALID_ARG;
+    return hip_status(qg::launch_linear_fp8(reinterpret_cast<const uint16_t*>(x), ldx, a_tensor_scale,
+                                            reinterpret_cast<const uint8_t*>(w_packed), m, n, k, y, ldy,
+                                            y_dtype == QG_OUT_F32 ? 1 : 0, reinterpret_cast<hipStream_t>(stream)));
+  }();
+  if (qg::log_enabled())
+    qg::log_call("qg_linear_fp8", st_, "m=%lld n=%lld k=%lld ldx=%lld ldy=%lld y_dtype=%d", (long long)m,
+                 (long long)n, (long long)k, (long long)ldx, (long long)ldy, (int)y_dtype);
   return st_;
 }
 

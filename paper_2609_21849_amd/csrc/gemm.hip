@@ -693,9 +693,17 @@ static hipError_t run_fp8(GemmArgs g, hipStream_t st) {
 // waves 0..NW/2-1 through it.
 // Tiles are dealt so that each XCD owns a contiguous range of weight panel
 // groups (its L2 then holds 1/8 of the weight and the whole activation).
-template <int MODE, int MT, int NP, int NW, int D>
+// AQ (FP8 only): A is the bf16 activation itself, quantized in the kernel.
+// Every workgroup first reduces the max of the whole activation (a small
+// one: the caller bounds it) and derives the decode scale exactly as the
+// dynamic quantizer does; each lane then codes the bf16 elements it loads
+// for a step into the E4M3 bytes the FP8 path would have loaded, so codes,
+// scale and accumulation order are those of quantize-then-GEMM. Workgroup 0
+// writes the scale to a_tscale.
+template <int MODE, int MT, int NP, int NW, int D, bool AQ = false>
 __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   static_assert(MODE == MODE_FP8 || MODE == MODE_NVFP4, "W8A8 or W4A4");
+  static_assert(!AQ || MODE == MODE_FP8, "in-kernel activation quantization: FP8");
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int BM = 32 * MT, BN = 32 * NP;
   constexpr int LDR = BN + 4;  // fp32 row pitch of a partial tile in LDS
@@ -725,7 +733,10 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   // NVFP4 activation rows: lda / 2 code bytes and lda / 16 scale bytes apart,
   // the descriptors ending at the last row's k / 2 and k / 16 bytes
   const int64_t ka = g.lda >> 1, ks = g.lda >> 4;
-  const __amdgpu_buffer_rsrc_t rs_a_ = (MODE == MODE_FP8)
+  const __amdgpu_buffer_rsrc_t rs_a_ = AQ
+      ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)(((int64_t)(g.m - 1) * g.lda + g.k) * 2),
+                                          0x00020000)
+      : (MODE == MODE_FP8)
       ? rsrc_a_fp8(g)
       : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.a), 0, (int)((int64_t)(g.m - 1) * ka + (g.k >> 1)),
                                           0x00020000);
@@ -741,7 +752,10 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   for (int i = 0; i < MT; ++i) {
     const int row = m0 + 32 * i + r;
     const bool in = row < g.m;
-    if (MODE == MODE_FP8) {
+    if (AQ) {  // bf16: two bytes per element
+      oa[i] = in ? (uint32_t)(((int64_t)row * g.lda + 32 * gq) * 2) : OOB;
+      oas[i] = OOB;
+    } else if (MODE == MODE_FP8) {
       oa[i] = in ? (uint32_t)((int64_t)row * g.lda + 32 * gq) : OOB;
       oas[i] = OOB;
     } else {
@@ -757,10 +771,13 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
     ows[j] = in ? (uint32_t)(pj * kcn * 256 + r * 8 + 4 * gq) : OOB;
   }
 
+  // AQ: the activation's decode scale and its reciprocal (set below)
+  float aq_s = 0.0f, aq_r = 0.0f;
+
   // one 128-wide chunk of a lane's operands; FP8: piece 2 s + h = step s,
   // register half h; NVFP4: pieces 0, 1 = the 32 code bytes, sc = 4 scales
   struct Chunk {
-    v4i a[MT][MODE == MODE_FP8 ? 4 : 2];
+    v4i a[MT][AQ ? 8 : (MODE == MODE_FP8 ? 4 : 2)];  // AQ: the bf16 elements of the FP8 pieces
     v4i w[NP][MODE == MODE_FP8 ? 4 : 2];
     uint32_t as[MODE == MODE_NVFP4 ? MT : 1];
     uint32_t ws[MODE == MODE_NVFP4 ? NP : 1];
@@ -778,8 +795,15 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {  // step p / 2, register half p % 2
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
-          C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + (p >> 1) * 64 + (p & 1) * 16, kq * 128, 0);
+        for (int i = 0; i < MT; ++i) {
+          if (AQ) {  // the 16 elements of piece p as bf16: two 16-byte loads
+            C.a[i][2 * p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + (p >> 1) * 128 + (p & 1) * 32, kq * 256, 0);
+            C.a[i][2 * p + 1] =
+                __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + (p >> 1) * 128 + (p & 1) * 32 + 16, kq * 256, 0);
+          } else {
+            C.a[i][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_a, oa[i] + (p >> 1) * 64 + (p & 1) * 16, kq * 128, 0);
+          }
+        }
 #pragma unroll
         for (int j = 0; j < NP; ++j)
           C.w[j][p] = __builtin_amdgcn_raw_buffer_load_b128(rs_w, ow[j] + p * 1024, kq * 4096, 0);
@@ -821,8 +845,23 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
         v8i fa[MT], fb[NP];
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
-          const v4i lo = C.a[i][2 * s], hi = C.a[i][2 * s + 1];
-          fa[i] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          if (AQ) {
+            // E4M3(fl(x r)), four elements per dword: the dynamic
+            // quantizer's element step
+            int q[8];
+#pragma unroll
+            for (int d = 0; d < 8; ++d) {
+              const v4i v = C.a[i][4 * s + (d >> 1)];
+              const uint32_t w0 = (uint32_t)((d & 1) ? v.z : v.x), w1 = (uint32_t)((d & 1) ? v.w : v.y);
+              const float y[4] = {__fmul_rn(bf16_lo(w0), aq_r), __fmul_rn(bf16_hi(w0), aq_r),
+                                  __fmul_rn(bf16_lo(w1), aq_r), __fmul_rn(bf16_hi(w1), aq_r)};
+              q[d] = (int)hw_e4m3x4(y);
+            }
+            fa[i] = (v8i){q[0], q[1], q[2], q[3], q[4], q[5], q[6], q[7]};
+          } else {
+            const v4i lo = C.a[i][2 * s], hi = C.a[i][2 * s + 1];
+            fa[i] = (v8i){lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          }
         }
 #pragma unroll
         for (int j = 0; j < NP; ++j) {
@@ -888,6 +927,43 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   Chunk C[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) load(C[d], wave + NW * d);
+  if constexpr (AQ) {
+    // max |x| over the whole activation (bf16 magnitude bits, as the
+    // quantizer reduces them), eight 16-byte units per thread in flight
+    // (sixteen were no faster at 128 x 256 and slower at 1 x 1024 .. 16 x 1024)
+    __shared__ uint32_t aq_part[NW];
+    const int upr = g.k >> 3, units = g.m * upr;
+    uint32_t mx = 0;
+    for (int u0 = (int)threadIdx.x; u0 < units; u0 += 8 * 64 * NW) {
+      uint4 v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int u = u0 + e * 64 * NW;
+        const int row = u / upr;
+        v[e] = (u < units) ? *reinterpret_cast<const uint4*>(g.a + ((int64_t)row * g.lda + 8 * (u - row * upr)) * 2)
+                           : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t w[4] = {v[e].x, v[e].y, v[e].z, v[e].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t t2 = w[j] & 0x7FFF7FFFu;
+          mx = max(mx, max(t2 & 0xFFFFu, t2 >> 16));
+        }
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+    if (lane == 0) aq_part[wave] = mx;
+    __syncthreads();
+    uint32_t a = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) a = max(a, aq_part[w]);
+    a <<= 16;
+    aq_s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), 448.0f);
+    aq_r = (aq_s > 0.0f) ? __fdiv_rn(1.0f, aq_s) : 0.0f;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *const_cast<float*>(g.a_tscale) = aq_s;
+  }
   for (int t0 = 0; t0 < nt; t0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
@@ -927,7 +1003,7 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   }
   if (wave < NRED) put(red + wave * (BM * LDR));
   __syncthreads();
-  const float c = *g.w_tscale * *g.a_tscale;
+  const float c = *g.w_tscale * (AQ ? aq_s : *g.a_tscale);
   const bool vec = out_vec(g);
   const float ry = out_rscale(g);
   const bool nv = g.out_mode == OUT_NVFP4;
@@ -952,11 +1028,11 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
   }
 }
 
-template <int MODE, int MT, int NP, int NW, int D>
+template <int MODE, int MT, int NP, int NW, int D, bool AQ = false>
 static hipError_t run_splitk(GemmArgs g, hipStream_t st) {
   g.tiles_m = (g.m + 32 * MT - 1) / (32 * MT);
   g.tiles_n = (g.n + 32 * NP - 1) / (32 * NP);
-  hipLaunchKernelGGL((k_gemm_splitk<MODE, MT, NP, NW, D>), dim3(g.tiles_m * g.tiles_n), dim3(64 * NW), 0, st, g);
+  hipLaunchKernelGGL((k_gemm_splitk<MODE, MT, NP, NW, D, AQ>), dim3(g.tiles_m * g.tiles_n), dim3(64 * NW), 0, st, g);
   return hipGetLastError();
 }
 
@@ -3062,6 +3138,62 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
     }
     return run<MODE_W4A16, 2, 2, 2, 4>(g, st);
   }
+}
+
+// The FP8 decode scale of a small bf16 activation alone (one workgroup):
+// the degenerate shapes of the fused linear, which launch no GEMM tile.
+__global__ void __launch_bounds__(256) k_fp8_scale_only(const uint16_t* __restrict__ x, int64_t m, int64_t k,
+                                                        int64_t ldx, float* __restrict__ s) {
+  uint32_t mx = 0;
+  for (int64_t i = threadIdx.x; i < m * k; i += 256) mx = max(mx, (uint32_t)(x[(i / k) * ldx + i % k] & 0x7FFFu));
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t a = max(max(part[0], part[1]), max(part[2], part[3])) << 16;
+    *s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), 448.0f);
+  }
+}
+
+hipError_t launch_linear_fp8(const uint16_t* x, int64_t ldx, float* a_tscale, const uint8_t* w_packed, int64_t m,
+                             int64_t n, int64_t k, void* y, int64_t ldy, int out_mode, hipStream_t st) {
+  if (m == 0 || n == 0 || k == 0) {
+    hipLaunchKernelGGL(k_fp8_scale_only, dim3(1), dim3(256), 0, st, x, m, k, ldx, a_tscale);
+    if (m > 0 && n > 0)
+      hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)((m * n + 255) / 256)), dim3(256), 0, st, y, nullptr, m, n,
+                         ldy, out_mode);
+    return hipGetLastError();
+  }
+  GemmArgs g;
+  g.a = reinterpret_cast<const uint8_t*>(x);
+  g.a_bscale = nullptr;
+  g.a_tscale = a_tscale;
+  g.lda = ldx;
+  g.w_codes = w_packed + kPackHeader;
+  g.w_scales = g.w_codes + packed_codes_bytes(1, n, k);
+  g.w_tscale = reinterpret_cast<const float*>(w_packed + kPackScaleOffset);
+  g.m = (int)m;
+  g.n = (int)n;
+  g.k = (int)k;
+  g.y = y;
+  g.ldy = ldy;
+  g.out_mode = out_mode;
+  g.y_scale = nullptr;
+  g.y_bscale = nullptr;
+  // the split-K tiling launch_gemm takes for an FP8 activation of this shape
+  // (so the accumulation order is the same), the 32 x 64 tiles with two
+  // chunks in flight where it would leave the split-K kernel
+  const int cus = device_cus();
+  const int64_t rows32 = (m + 31) / 32;
+  if (rows32 * ((n + 31) / 32) <= cus) {
+    if ((k >> 7) <= 4) return run_splitk<MODE_FP8, 1, 1, 4, 1, true>(g, st);
+    return run_splitk<MODE_FP8, 1, 1, 8, 1, true>(g, st);
+  }
+  if (rows32 * ((n + 63) / 64) <= cus) return run_splitk<MODE_FP8, 1, 2, 4, 2, true>(g, st);
+  if (rows32 * ((n + 95) / 96) <= cus) return run_splitk<MODE_FP8, 1, 3, 8, 1, true>(g, st);
+  if (rows32 * ((n + 127) / 128) <= cus) return run_splitk<MODE_FP8, 1, 4, 8, 1, true>(g, st);
+  return run_splitk<MODE_FP8, 1, 2, 4, 2, true>(g, st);
 }
 
 }  // namespace qg

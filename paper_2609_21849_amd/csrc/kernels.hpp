@@ -51,5 +51,10 @@ hipError_t launch_gemm(int a_fmt, const void* a, const uint8_t* a_bscale, const 
                        int64_t lda, const uint8_t* w_packed, int64_t m, int64_t n, int64_t k,
                        void* y, int64_t ldy, int out_mode, const float* y_scale, uint8_t* y_bscale,
                        hipStream_t st);
+// W8A8 linear from bf16 activations x [m, ldx] (16-byte aligned rows):
+// the dynamic FP8 quantization of x inside the split-K GEMM; a_tscale
+// receives the decode scale; out_mode 0 (bf16) or 1 (fp32)
+hipError_t launch_linear_fp8(const uint16_t* x, int64_t ldx, float* a_tscale, const uint8_t* w_packed, int64_t m,
+                             int64_t n, int64_t k, void* y, int64_t ldy, int out_mode, hipStream_t st);
 
 }  // namespace qg

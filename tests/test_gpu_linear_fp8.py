@@ -1,0 +1,121 @@
+"""GPU parity of qg_linear_fp8, the W8A8 linear that quantizes its bf16
+activation inside the GEMM: the decode scale must carry the bits
+qg_quantize_act writes, and the output must equal quantize-then-qg_gemm
+bit for bit on the shapes where qg_gemm takes the same split-K tiling (and
+meet the 1e-3 sum|a w| bound against the oracle everywhere)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_21849_amd as q
+import synth
+from gpu_util import DEV, check_linear, host, log, scale_of, to_dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+FP8 = q.QG_FMT_FP8_E4M3
+STATUS = {v: k for k, v in q.STATUS_NAMES.items()}
+
+
+def _packed(w):
+    wq = q.quantize(to_dev_bf16(w), FP8)
+    return q.pack(wq)
+
+
+def _unfused(xd, packed, n, out):
+    a = q.quantize(xd, FP8)
+    y = q.linear(a, packed, FP8, n, out_dtype=out)
+    return y, a.tensor_scale
+
+
+# (m, n, k) and the split-K tiling both paths take: the single FP8 linear,
+# encoder linears at few tokens, ragged rows, the 32 x 64 / 96 / 128 tilings
+# and the largest activation (m k = 65536)
+SHAPES = [(128, 256, 256), (16, 1024, 3072), (16, 3072, 1024), (1, 3072, 1024), (64, 1024, 1024),
+          (200, 256, 256), (37, 4096, 128), (512, 1024, 128), (256, 2048, 256), (128, 6144, 512),
+          (128, 8192, 512), (21, 16, 3072)]
+
+
+@pytest.mark.parametrize("m,n,k", SHAPES)
+@pytest.mark.parametrize("out", [q.QG_OUT_BF16, q.QG_OUT_F32])
+def test_equals_quantize_then_gemm(m, n, k, out):
+    log("linear_fp8 m=%d n=%d k=%d out=%d" % (m, n, k, out))
+    x = synth.normal_bf16(m, k, 1.0, 21, 0, outlier_frac=0.001, outlier_gain=50.0)
+    w = synth.normal_bf16(n, k, 0.02, 21, 1)
+    xd, packed = to_dev_bf16(x), _packed(w)
+    y, ts = q.linear_fp8(xd, packed, n, out)
+    y_ref, ts_ref = _unfused(xd, packed, n, out)
+    torch.cuda.synchronize()
+    assert host(ts).view(np.uint32)[0] == host(ts_ref).view(np.uint32)[0]
+    assert torch.equal(y.view(torch.int32 if out == q.QG_OUT_F32 else torch.int16),
+                       y_ref.view(torch.int32 if out == q.QG_OUT_F32 else torch.int16))
+
+
+def test_single_fp8_linear_against_the_oracle():
+    # the single FP8 linear (128 x 256 x 256), every output, both output types
+    x = synth.normal_bf16(128, 256, 1.0, 0, 0)
+    w = synth.normal_bf16(256, 256, 0.02, 0, 1)
+    packed = _packed(w)
+    ref = oracle.linear_reference("fp8", x, w)
+    y, ts = q.linear_fp8(to_dev_bf16(x), packed, 256)
+    y32, _ = q.linear_fp8(to_dev_bf16(x), packed, 256, q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    _, s = oracle.quantize_fp8(x)
+    assert scale_of(ts).view(np.uint32) == np.float32(s).view(np.uint32)
+    log("fused C1 max err/B", check_linear(y, ref, name="C1 fp8 w8a8 128x256x256 fused quantize (every output)"))
+    check_linear(y32, ref)
+
+
+def test_wide_output_leaves_the_shared_tiling():
+    # 16 x 40960 x 128: qg_gemm leaves the split-K kernel here, the fused
+    # linear keeps 32 x 64 tiles; both within the bound of the oracle
+    m, n, k = 16, 40960, 128
+    x = synth.normal_bf16(m, k, 1.0, 22, 0)
+    w = synth.normal_bf16(n, k, 0.02, 22, 1)
+    y, _ = q.linear_fp8(to_dev_bf16(x), _packed(w), n, q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    check_linear(y, oracle.linear_reference("fp8", x, w))
+
+
+@pytest.mark.parametrize("bad", [0x7F80, 0xFFC1])
+def test_nonfinite_activation(bad):
+    # inf or NaN: NaN scale and NaN outputs, as quantize-then-GEMM gives
+    m, n, k = 16, 256, 256
+    x = synth.normal_bf16(m, k, 1.0, 23, 0)
+    x[3, 100] = bad
+    w = synth.normal_bf16(n, k, 0.02, 23, 1)
+    y, ts = q.linear_fp8(to_dev_bf16(x), _packed(w), n, q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    assert np.isnan(scale_of(ts))
+    assert np.all(np.isnan(host(y)))
+
+
+def test_zero_activation_and_empty_shapes():
+    n, k = 256, 256
+    w = synth.normal_bf16(n, k, 0.02, 24, 1)
+    packed = _packed(w)
+    y, ts = q.linear_fp8(torch.zeros((8, k), dtype=torch.bfloat16, device=DEV), packed, n, q.QG_OUT_F32)
+    torch.cuda.synchronize()
+    assert scale_of(ts) == 0.0 and not np.any(host(y))
+    ts2 = torch.full((1,), 7.0, dtype=torch.float32, device=DEV)
+    x = to_dev_bf16(synth.normal_bf16(4, k, 1.0, 24, 0))
+    q.qg_linear_fp8(x, k, ts2, packed, packed.numel(), 4, 0, k, None, 0, q.QG_OUT_BF16)   # n = 0: the scale only
+    torch.cuda.synchronize()
+    assert scale_of(ts2) == scale_of(q.quantize(x, FP8).tensor_scale)
+
+
+def test_argument_checks():
+    n, k = 256, 256
+    packed = _packed(synth.normal_bf16(n, k, 0.02, 25, 1))
+    x = torch.zeros((300, k), dtype=torch.bfloat16, device=DEV)   # m k = 76800 > 65536
+    y = torch.empty((300, n), dtype=torch.bfloat16, device=DEV)
+    ts = torch.empty(1, dtype=torch.float32, device=DEV)
+    s = q.qg_linear_fp8(x, k, ts, packed, packed.numel(), 300, n, k, y, n, q.QG_OUT_BF16, check=False)
+    assert s == STATUS["QG_ERR_SHAPE"]
+    s = q.qg_linear_fp8(x, k, None, packed, packed.numel(), 16, n, k, y, n, q.QG_OUT_BF16, check=False)
+    assert s == STATUS["QG_ERR_INVALID_ARG"]
+    s = q.qg_linear_fp8(x, k, ts, packed, packed.numel() - 1, 16, n, k, y, n, q.QG_OUT_BF16, check=False)
+    assert s == STATUS["QG_ERR_BUFFER_TOO_SMALL"]
+    s = q.qg_linear_fp8(x[:, 1:], k, ts, packed, packed.numel(), 16, n, k - 128, y, n, q.QG_OUT_BF16, check=False)
+    assert s == STATUS["QG_ERR_INVALID_ARG"]   # 2-byte aligned rows

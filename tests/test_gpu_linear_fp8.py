@@ -52,6 +52,20 @@ def test_equals_quantize_then_gemm(m, n, k, out):
                        y_ref.view(torch.int32 if out == q.QG_OUT_F32 else torch.int16))
 
 
+@pytest.mark.parametrize("m,n,k,pad", [(16, 1024, 1024, 64), (100, 512, 256, 8)])
+def test_row_stride_larger_than_row(m, n, k, pad):
+    # the first k columns of a wider activation (ldx = k + pad) in place
+    full = synth.normal_bf16(m, k + pad, 1.0, 26, 0, outlier_frac=0.001, outlier_gain=50.0)
+    xd = to_dev_bf16(full)[:, :k]
+    assert xd.stride(0) == k + pad
+    packed = _packed(synth.normal_bf16(n, k, 0.02, 26, 1))
+    y, ts = q.linear_fp8(xd, packed, n)
+    y_ref, ts_ref = _unfused(xd, packed, n, q.QG_OUT_BF16)
+    torch.cuda.synchronize()
+    assert host(ts).view(np.uint32)[0] == host(ts_ref).view(np.uint32)[0]
+    assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+
+
 def test_single_fp8_linear_against_the_oracle():
     # the single FP8 linear (128 x 256 x 256), every output, both output types
     x = synth.normal_bf16(128, 256, 1.0, 0, 0)

@@ -4,12 +4,15 @@
 // linears of the paper's denoising transformer (Sec. 4, quantization
 // paragraph; Table 2) and of its small text encoder (weight-only).
 //
-// Three operand modes, all on 32x32 MFMAs:
+// Three operand modes:
 //   W8A8  (FP8 x FP8)    : codes go straight into v_mfma_f32_32x32x64_f8f6f4
-//                          (OCP E4M3 operands); tensor scales in the epilogue.
-//                          Kernels: k_gemm_fp8_direct for large token
-//                          counts, k_gemm_fp8 for mid-size ones, the split-K
-//                          k_gemm_splitk for few tokens.
+//                          (OCP E4M3 operands; v_mfma_f32_16x16x128_f8f6f4 in
+//                          the 288 x 192 tile kernel); tensor scales in the
+//                          epilogue. Kernels: k_gemm_fp8_t288 and
+//                          k_gemm_fp8_direct for large token counts, k_gemm_fp8
+//                          for mid-size ones, the split-K k_gemm_splitk for few
+//                          tokens (also from a bf16 activation quantized in the
+//                          kernel: qg_linear_fp8).
 //   W4A4  (NVFP4 x NVFP4): the E4M3 block scale changes every 16 reduction
 //                          elements and is not a power of two, so it cannot
 //                          ride in the hardware's per-32 power-of-two operand
@@ -771,8 +774,12 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
     ows[j] = in ? (uint32_t)(pj * kcn * 256 + r * 8 + 4 * gq) : OOB;
   }
 
-  // AQ: the activation's decode scale and its reciprocal (set below)
+  // AQ: the activation's decode scale and its reciprocal (set below); with
+  // a finite r every |x r| stays below 464 (x r <= max|x| r, within a few
+  // ulps of 448), where the hardware conversion rounds as the clamped one
+  // does, so the clamp is kept only for r = inf (a max below ~2^-119)
   float aq_s = 0.0f, aq_r = 0.0f;
+  bool aq_clamp = false;
 
   // one 128-wide chunk of a lane's operands; FP8: piece 2 s + h = step s,
   // register half h; NVFP4: pieces 0, 1 = the 32 code bytes, sc = 4 scales
@@ -849,13 +856,28 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
             // E4M3(fl(x r)), four elements per dword: the dynamic
             // quantizer's element step
             int q[8];
+            if (aq_clamp) {
 #pragma unroll
-            for (int d = 0; d < 8; ++d) {
-              const v4i v = C.a[i][4 * s + (d >> 1)];
-              const uint32_t w0 = (uint32_t)((d & 1) ? v.z : v.x), w1 = (uint32_t)((d & 1) ? v.w : v.y);
-              const float y[4] = {__fmul_rn(bf16_lo(w0), aq_r), __fmul_rn(bf16_hi(w0), aq_r),
-                                  __fmul_rn(bf16_lo(w1), aq_r), __fmul_rn(bf16_hi(w1), aq_r)};
-              q[d] = (int)hw_e4m3x4(y);
+              for (int d = 0; d < 8; ++d) {
+                const v4i v = C.a[i][4 * s + (d >> 1)];
+                const uint32_t w0 = (uint32_t)((d & 1) ? v.z : v.x), w1 = (uint32_t)((d & 1) ? v.w : v.y);
+                const float y[4] = {__fmul_rn(bf16_lo(w0), aq_r), __fmul_rn(bf16_hi(w0), aq_r),
+                                    __fmul_rn(bf16_lo(w1), aq_r), __fmul_rn(bf16_hi(w1), aq_r)};
+                q[d] = (int)hw_e4m3x4(y);
+              }
+            } else {
+#pragma unroll
+              for (int d = 0; d < 8; ++d) {
+                const v4i v = C.a[i][4 * s + (d >> 1)];
+                const uint32_t w0 = (uint32_t)((d & 1) ? v.z : v.x), w1 = (uint32_t)((d & 1) ? v.w : v.y);
+                typedef short v2s __attribute__((ext_vector_type(2)));
+                v2s c = {0, 0};
+                c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, __fmul_rn(bf16_lo(w0), aq_r),
+                                                             __fmul_rn(bf16_hi(w0), aq_r), 1.0f, false);
+                c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, __fmul_rn(bf16_lo(w1), aq_r),
+                                                             __fmul_rn(bf16_hi(w1), aq_r), 1.0f, true);
+                q[d] = __builtin_bit_cast(int, c);
+              }
             }
             fa[i] = (v8i){q[0], q[1], q[2], q[3], q[4], q[5], q[6], q[7]};
           } else {
@@ -962,6 +984,7 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_splitk(GemmArgs g) {
     a <<= 16;
     aq_s = (a >= 0x7F800000u) ? __builtin_nanf("") : __fdiv_rn(u2f(a), 448.0f);
     aq_r = (aq_s > 0.0f) ? __fdiv_rn(1.0f, aq_s) : 0.0f;
+    aq_clamp = !(aq_r <= 3.40282347e38f);
     if (blockIdx.x == 0 && threadIdx.x == 0) *const_cast<float*>(g.a_tscale) = aq_s;
   }
   for (int t0 = 0; t0 < nt; t0 += D) {

@@ -92,6 +92,24 @@ def test_wide_output_leaves_the_shared_tiling():
     check_linear(y, oracle.linear_reference("fp8", x, w))
 
 
+@pytest.mark.parametrize("gain", [2.0 ** -100, 2.0 ** -118, 2.0 ** -122, 2.0 ** -128])
+def test_tiny_activations(gain):
+    # a max below ~2^-119 makes r = 1/s overflow to inf (then the codes need
+    # the quantizer's clamp); just above it r is finite but huge
+    m, n, k = 16, 256, 512
+    xf = synth.bf16_bits_to_f32(synth.normal_bf16(m, k, 1.0, 27, 0)).astype(np.float64) * gain
+    x = synth.f32_to_bf16_bits(xf.astype(np.float32))
+    packed = _packed(synth.normal_bf16(n, k, 0.02, 27, 1))
+    xd = to_dev_bf16(x)
+    for out in (q.QG_OUT_F32, q.QG_OUT_BF16):
+        y, ts = q.linear_fp8(xd, packed, n, out)
+        y_ref, ts_ref = _unfused(xd, packed, n, out)
+        torch.cuda.synchronize()
+        assert host(ts).view(np.uint32)[0] == host(ts_ref).view(np.uint32)[0]
+        iv = torch.int32 if out == q.QG_OUT_F32 else torch.int16
+        assert torch.equal(y.view(iv), y_ref.view(iv))
+
+
 @pytest.mark.parametrize("bad", [0x7F80, 0xFFC1])
 def test_nonfinite_activation(bad):
     # inf or NaN: NaN scale and NaN outputs, as quantize-then-GEMM gives

@@ -54,6 +54,11 @@ def parse():
     ap.add_argument("--stall-summary", nargs=2, metavar=("PMC_DIRS", "OUT_MD"),
                     help="turn the counter passes STALL_PASSES over --traffic-probe (directories comma-separated) "
                          "into the wave-time summary")
+    ap.add_argument("--quant-probe", action="store_true",
+                    help="only the dynamic activation quantizers (FP8 and NVFP4, 4608 x 3072 and 4608 x 9216, "
+                         "3x each) and a calibration copy; for rocprofv3 runs")
+    ap.add_argument("--quant-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "TRACE_DIR", "OUT_MD"),
+                    help="turn two counter runs and a kernel trace of --quant-probe into the quantizer summary")
     ap.add_argument("--kind", choices=("nvfp4", "fp8"), default="nvfp4",
                     help="format of the --traffic-summary / --mfma-summary counter runs")
     ap.add_argument("--w4a16-pool-only", action="store_true",
@@ -123,6 +128,117 @@ def traffic_probe(kind):
         dst.copy_(src)
     torch.cuda.synchronize()
     print("traffic probe done", flush=True)
+
+
+QUANT_SHAPES = ((4608, 3072), (4608, 9216))   # the transformer linears' two activation sizes
+QUANT_KERNELS = ("k_amax_dense", "k_finalize", "k_quant_dense")
+
+
+def quant_probe():
+    """The dynamic quantizers of the step's activations: FP8 (N(0,1)) and
+    NVFP4 (heavy-tailed), each size three times, then the calibration copy."""
+    import torch
+    import paper_2609_21849_amd as q
+    import synth
+    torch.cuda.set_device(0)
+    for fmt, tail in ((q.QG_FMT_FP8_E4M3, 0.0), (q.QG_FMT_NVFP4, synth.HEAVY_TAIL_FRAC)):
+        for (m, k) in QUANT_SHAPES:
+            x = dev_bf16(synth.normal_bf16(m, k, synth.SIGMA_X, 0, synth.STREAM_X, outlier_frac=tail,
+                                           outlier_gain=synth.HEAVY_TAIL_GAIN, outlier_stream=synth.STREAM_OUTLIER))
+            qt = q.quantize(x, fmt)
+            torch.cuda.synchronize()
+            for _ in range(3):
+                q.qg_quantize_act(fmt, x, m, k, k, qt.codes, qt.block_scales, qt.tensor_scale)
+            torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print("quant probe done", flush=True)
+
+
+def quant_summary(fetch_dir, write_dir, trace_dir, out_md):
+    """HBM bytes and rates of the three quantizer kernels at the step's
+    activation sizes: FETCH_SIZE / WRITE_SIZE per dispatch (copy-calibrated
+    as for the GEMMs) and durations from a kernel trace of the same probe;
+    the rate is the algorithmic bytes over the kernel's duration."""
+    import csv
+    import glob
+    rows = {}
+    for ctr, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rs = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rs += [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == ctr]
+        rs.sort(key=lambda r: int(r.get("Dispatch_Id", 0)))
+        rows[ctr] = rs
+    tr = []
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        tr += list(csv.DictReader(open(f)))
+    tr.sort(key=lambda t: int(t["Start_Timestamp"]))
+
+    def seq(items, name_of):
+        out = {kname: [] for kname in QUANT_KERNELS}
+        copy = []
+        for it in items:
+            n = name_of(it)
+            for kname in QUANT_KERNELS:
+                if kname + "(" in n or kname + "<" in n:
+                    out[kname].append(it)
+            if "copyBuffer" in n or "copy_kernel" in n:
+                copy.append(it)
+        return out, copy
+    fk, fc = seq(rows["FETCH_SIZE"], lambda r: r["Kernel_Name"])
+    wk, wc = seq(rows["WRITE_SIZE"], lambda r: r["Kernel_Name"])
+    tk, _ = seq(tr, lambda t: t["Kernel_Name"])
+    ncalls = 2 * len(QUANT_SHAPES) * 3
+    # q.quantize() before each size's three timed calls adds one call per size
+    per_size = 4
+    for kname in QUANT_KERNELS:
+        assert len(fk[kname]) == len(wk[kname]) == len(tk[kname]) == 2 * len(QUANT_SHAPES) * per_size, \
+            (kname, len(fk[kname]), len(wk[kname]), len(tk[kname]), ncalls)
+    f_factor = sum(float(r["Counter_Value"]) for r in fc) / len(fc) * 1024 / COPY_BYTES
+    w_factor = sum(float(r["Counter_Value"]) for r in wc) / len(wc) * 1024 / COPY_BYTES
+    lines = ["# The dynamic activation quantizers at the transformer activation sizes", "",
+             "The three kernels of a dynamic per-tensor quantization of a 4608 x 3072 and a 4608 x 9216 bf16 "
+             "activation (FP8: N(0,1); NVFP4: heavy-tailed), each call three times after one warm-up call: HBM "
+             "bytes per dispatch from FETCH_SIZE and WRITE_SIZE (each scaled by what it reads for a %d MiB "
+             "device-to-device copy: fetch factor %.4f, write factor %.4f), kernel durations from a kernel "
+             "trace of the same probe (mean of the three timed calls). Algorithmic bytes: amax reads the "
+             "activation (2 bytes per element); finalize reads the partial maxima; quantize reads the activation "
+             "and writes the codes (FP8 1 byte per element, NVFP4 0.5 plus 1/16 of block scales). The rate is "
+             "algorithmic bytes over duration, against the 8 TB/s HBM peak." % (COPY_BYTES >> 20, f_factor, w_factor),
+             "", "Commands (repo root, MI355X; $OUT any output directory):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE "
+             "--output-format csv -d $OUT/pmc_fetch_quant -o run -- python3 bench.py --quant-probe",
+             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE "
+             "--output-format csv -d $OUT/pmc_write_quant -o run -- python3 bench.py --quant-probe",
+             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --kernel-trace "
+             "--output-format csv -d $OUT/trace_quant -o run -- python3 bench.py --quant-probe",
+             "python3 bench.py --quant-summary $OUT/pmc_fetch_quant $OUT/pmc_write_quant $OUT/trace_quant <this file>",
+             "```", "",
+             "| format | activation | kernel | fetch MB | write MB | algorithmic MB | duration us | GB/s | of 8 TB/s |",
+             "|---|---|---|---:|---:|---:|---:|---:|---:|"]
+    i = 0
+    for fname in ("FP8", "NVFP4"):
+        for (m, k) in QUANT_SHAPES:
+            n = m * k
+            alg = {"k_amax_dense": 2.0 * n, "k_finalize": 4096.0,
+                   "k_quant_dense": 2.0 * n + (n if fname == "FP8" else n / 2 + n / 16)}
+            for kname in QUANT_KERNELS:
+                sl = slice(per_size * i + 1, per_size * i + per_size)   # the three timed calls
+                fb = sum(float(r["Counter_Value"]) for r in fk[kname][sl]) / 3 * 1024 / f_factor
+                wb = sum(float(r["Counter_Value"]) for r in wk[kname][sl]) / 3 * 1024 / w_factor
+                us = sum(int(t["End_Timestamp"]) - int(t["Start_Timestamp"]) for t in tk[kname][sl]) / 3 / 1e3
+                gbs = alg[kname] / (us * 1e3)
+                lines.append("| %s | %d x %d | `%s` | %.1f | %.1f | %.1f | %.2f | %.0f | %.3f |"
+                             % (fname, m, k, kname, fb / 1e6, wb / 1e6, alg[kname] / 1e6, us, gbs, gbs / PEAK["hbm_gbs"]))
+            i += 1
+    lines += ["", "Source: paper_2609_21849_amd/csrc/quantize.hip.", ""]
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
 
 
 def read_counter(d, counter, kernel):
@@ -335,6 +451,12 @@ def main():
         return
     if args.stall_summary:
         stall_summary(*args.stall_summary, kind=args.kind)
+        return
+    if args.quant_summary:
+        quant_summary(*args.quant_summary)
+        return
+    if args.quant_probe:
+        quant_probe()
         return
     if args.traffic_probe:
         traffic_probe(args.traffic_probe)

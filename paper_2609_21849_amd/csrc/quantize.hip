@@ -348,43 +348,60 @@ __global__ void __launch_bounds__(1024) k_quant_small(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------- dense tensors
-// Codes of one whole 16-byte unit (8 consecutive elements, index u) held in
-// `raw`: FP8 one 8-byte store, NVFP4 one 4-byte store plus, on the even lane
-// of a lane pair, the block scale (lanes 2j and 2j+1 hold the two halves of
-// one 16-element block and share its max with one lane swap, so every lane
-// of the wave must call this together; `in` only gates the stores).
-template <int FMT>
-__device__ inline void code_unit8(const uint4 raw, int64_t u, bool in, uint8_t* __restrict__ q,
-                                  uint8_t* __restrict__ bscale, float s, float r, float d_t, int lane) {
+// FP8 codes of one whole 16-byte unit (8 consecutive elements, index u)
+// held in `raw`: one 8-byte store, gated by `in`.
+__device__ inline void code_unit8_fp8(const uint4 raw, int64_t u, bool in, uint8_t* __restrict__ q, float r) {
   const uint32_t ww[4] = {raw.x, raw.y, raw.z, raw.w};
-  float v[8];
+  float y[8];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    v[2 * j] = bf16_lo(ww[j]);
-    v[2 * j + 1] = bf16_hi(ww[j]);
+    y[2 * j] = __fmul_rn(bf16_lo(ww[j]), r);
+    y[2 * j + 1] = __fmul_rn(bf16_hi(ww[j]), r);
   }
-  if (FMT == 1) {
+  const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
+  if (in) *reinterpret_cast<uint2*>(q + u * 8) = make_uint2(lo, hi);
+}
+
+// NVFP4 codes of two whole units per lane from two load steps: lanes 2j and
+// 2j+1 hold the halves of block A (units u[0]) and of block B (units u[1]);
+// the even lane derives A's scale, the odd lane B's, so each lane does one
+// block's two divisions for two blocks' worth of elements, and the two
+// reciprocals are swapped across the pair. Every lane of the wave calls it
+// together; in[] only gates the stores. The arithmetic of quant_nvfp4_words.
+__device__ inline void code_units8_nv_pair(const uint4 (&raw)[2], const int64_t (&u)[2], const bool (&in)[2],
+                                           uint8_t* __restrict__ q, uint8_t* __restrict__ bscale, float s,
+                                           float d_t, int lane) {
+  float v[2][8];
+  uint32_t am[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const uint32_t ww[4] = {raw[p].x, raw[p].y, raw[p].z, raw[p].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[p][2 * j] = bf16_lo(ww[j]);
+      v[p][2 * j + 1] = bf16_hi(ww[j]);
+    }
+    uint32_t a = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a = max(a, f2u(v[p][j]) & 0x7FFFFFFFu);
+    am[p] = max(a, (uint32_t)__shfl_xor((int)a, 1));
+  }
+  const bool odd = lane & 1;
+  const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(odd ? am[1] : am[0]), d_t) : 0.0f;
+  const uint32_t sb = enc_e4m3(vb);
+  const float S = __fmul_rn(dec_e4m3(sb), s);
+  const float rb = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
+  const float rp = __shfl_xor(rb, 1);
+  const float rr[2] = {odd ? rp : rb, odd ? rb : rp};
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
     float y[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], r);
-    const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
-    if (in) *reinterpret_cast<uint2*>(q + u * 8) = make_uint2(lo, hi);
-  } else {
-    uint32_t am = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) am = max(am, f2u(v[j]) & 0x7FFFFFFFu);
-    am = max(am, (uint32_t)__shfl_xor((int)am, 1));
-    const float vb = (d_t > 0.0f) ? __fdiv_rn(u2f(am), d_t) : 0.0f;
-    const uint32_t sb = enc_e4m3(vb);
-    const float S = __fmul_rn(dec_e4m3(sb), s);
-    const float rb = (S > 0.0f) ? __fdiv_rn(1.0f, S) : 0.0f;
-    float y[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[j], rb);
+    for (int j = 0; j < 8; ++j) y[j] = __fmul_rn(v[p][j], rr[p]);
     const uint32_t w = hw_e2m1x8(y);
-    if (in) {
-      *reinterpret_cast<uint32_t*>(q + u * 4) = w;
-      if ((lane & 1) == 0) bscale[u >> 1] = (uint8_t)sb;
+    if (in[p]) {
+      *reinterpret_cast<uint32_t*>(q + u[p] * 4) = w;
+      if (odd == (p == 1)) bscale[u[p] >> 1] = (uint8_t)sb;
     }
   }
 }
@@ -397,7 +414,8 @@ __device__ inline void code_unit8(const uint4 raw, int64_t u, bool in, uint8_t* 
 // per lane are in flight. Elements are coded with the hardware conversions
 // (hw_e4m3x4 / hw_e2m1x8). NVFP4: n % 16 == 0, so lanes (2j, 2j+1) hold one
 // whole 16-element block (or both lie past the end); the block max is shared
-// with one lane swap.
+// with one lane swap, and each lane of the pair derives the scale of one of
+// the two blocks the pair holds in two consecutive steps.
 template <int FMT, int H>
 __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict__ x, int64_t n,
                                                      uint8_t* __restrict__ q,
@@ -414,17 +432,29 @@ __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict_
   const float s = *tscale;
   const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
   const float d_t = __fmul_rn(6.0f, s);
+  if constexpr (FMT == 2) {
+    static_assert(H % 2 == 0, "NVFP4 steps go in pairs");
 #pragma unroll
-  for (int h = 0; h < H; ++h) {
-    const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
-    const bool full = (e0 + 8 <= n);
-    code_unit8<FMT>(raw[h], e0 >> 3, full, q, bscale, s, r, d_t, lane);
-    if (FMT == 1 && !full && e0 < n) {  // FP8 tail unit of fewer than 8 elements
-      float y[8];
+    for (int h = 0; h < H; h += 2) {
+      const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
+      const uint4 rw[2] = {raw[h], raw[h + 1]};
+      const int64_t u[2] = {e0 >> 3, (e0 + 512) >> 3};
+      const bool in[2] = {e0 + 8 <= n, e0 + 520 <= n};
+      code_units8_nv_pair(rw, u, in, q, bscale, s, d_t, lane);
+    }
+  } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = (e0 + j < n) ? __fmul_rn(u2f((uint32_t)x[e0 + j] << 16), r) : 0.0f;
-      const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
-      for (int j = 0; j < 8 && e0 + j < n; ++j) q[e0 + j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
+    for (int h = 0; h < H; ++h) {
+      const int64_t e0 = chunk * (512 * H) + h * 512 + lane * 8;
+      const bool full = (e0 + 8 <= n);
+      code_unit8_fp8(raw[h], e0 >> 3, full, q, r);
+      if (!full && e0 < n) {  // FP8 tail unit of fewer than 8 elements
+        float y[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = (e0 + j < n) ? __fmul_rn(u2f((uint32_t)x[e0 + j] << 16), r) : 0.0f;
+        const uint32_t lo = hw_e4m3x4(y), hi = hw_e4m3x4(y + 4);
+        for (int j = 0; j < 8 && e0 + j < n; ++j) q[e0 + j] = (uint8_t)(((j < 4 ? lo : hi) >> (8 * (j & 3))) & 0xFFu);
+      }
     }
   }
 }
@@ -520,10 +550,21 @@ __global__ void __launch_bounds__(256) k_quant_dense_slots(const uint16_t* __res
   const float r = (FMT == 1 && s > 0.0f) ? __fdiv_rn(1.0f, s) : 0.0f;
   const float d_t = __fmul_rn(6.0f, s);
   for (int64_t base = lo;;) {
+    if constexpr (FMT == 2) {
 #pragma unroll
-    for (int h = 0; h < H; ++h) {
-      const int64_t u = base + 256 * wv + 64 * h + lane;
-      code_unit8<FMT>(raw[h], u, u < hi, q, bscale, s, r, d_t, lane);
+      for (int h = 0; h < H; h += 2) {
+        const int64_t u0 = base + 256 * wv + 64 * h + lane;
+        const uint4 rw[2] = {raw[h], raw[h + 1]};
+        const int64_t u[2] = {u0, u0 + 64};
+        const bool in[2] = {u0 < hi, u0 + 64 < hi};
+        code_units8_nv_pair(rw, u, in, q, bscale, s, d_t, lane);
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < H; ++h) {
+        const int64_t u = base + 256 * wv + 64 * h + lane;
+        code_unit8_fp8(raw[h], u, u < hi, q, r);
+      }
     }
     base += 1024;
     if (base >= hi) break;

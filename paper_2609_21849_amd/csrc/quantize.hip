@@ -11,8 +11,8 @@
 // one launch (k_quant_small); a dense one of at most 3 Mi elements in two
 // (k_amax_slots, k_quant_dense_slots: the maxima handed over inside the code
 // buffer); any other is a short chain on the caller's stream:
-//   k_amax_partial : max |x| as an integer max of bf16 magnitude bits (the
-//                    bit pattern of a non-negative value orders like the
+//   k_amax_dense / : max |x| as an integer max of bf16 magnitude bits (the
+//   k_amax_partial   bit pattern of a non-negative value orders like the
 //                    value); one partial per workgroup, parked in the code
 //                    buffer that the last kernel overwrites anyway
 //   k_finalize     : max of the partials -> decode scale s or s_t

@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-mib", type=int, default=600,
                     help="size of the weight pool for the cold-HBM W4A16 measurement")
-    ap.add_argument("--traffic-probe", nargs="?", const="nvfp4", choices=("nvfp4", "fp8"),
+    ap.add_argument("--traffic-probe", nargs="?", const="nvfp4", choices=("nvfp4", "fp8", "mxfp4", "mxfp8"),
                     help="only launch the DiT GEMMs of one format (3x per shape) and a calibration copy; "
                          "for rocprofv3 --pmc runs")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT_MD"),
@@ -59,7 +59,7 @@ def parse():
                          "3x each) and a calibration copy; for rocprofv3 runs")
     ap.add_argument("--quant-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "TRACE_DIR", "OUT_MD"),
                     help="turn two counter runs and a kernel trace of --quant-probe into the quantizer summary")
-    ap.add_argument("--kind", choices=("nvfp4", "fp8"), default="nvfp4",
+    ap.add_argument("--kind", choices=("nvfp4", "fp8", "mxfp4", "mxfp8"), default="nvfp4",
                     help="format of the --traffic-summary / --mfma-summary counter runs")
     ap.add_argument("--w4a16-pool-only", action="store_true",
                     help="only the cold-HBM W4A16 pool measurement (one JSON line); for rocprofv3 runs")
@@ -71,7 +71,12 @@ def parse():
 # only while the kernel source is the one the counters were taken on.
 TRAFFIC_MD = {"nvfp4": os.path.join(ROOT, "profiles", "k_gemm_nvfp4_direct_dit_traffic.md"),
               "fp8": os.path.join(ROOT, "profiles", "k_gemm_fp8_t288_dit_traffic.md")}
-KERNEL = {"nvfp4": "k_gemm_nvfp4_direct", "fp8": "k_gemm_fp8_t288"}
+KERNEL = {"nvfp4": "k_gemm_nvfp4_direct", "fp8": "k_gemm_fp8_t288", "mxfp4": "k_gemm_mxfp4_direct",
+          "mxfp8": "k_gemm_mxfp8_direct"}
+# executed-MFMA counter per format (none is known to count the fp4 operand
+# instructions, so the MXFP4 summary has MfmaUtil and the clock only)
+FLOPS_CTR = {"nvfp4": "MfmaFlopsF16", "fp8": "SQ_INSTS_VALU_MFMA_MOPS_F8", "mxfp8": "SQ_INSTS_VALU_MFMA_MOPS_F8",
+             "mxfp4": None}
 # counter passes of --stall-summary (each within one pass's per-block counter limits)
 STALL_PASSES = (
     "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
@@ -91,9 +96,9 @@ def source_sha() -> str:
 
 
 def gemm_bytes(kind, m, n, k):
-    """Algorithmic bytes of one DiT GEMM: A codes (+ NVFP4 block scales),
-    packed W codes (+ scales), bf16 Y."""
-    per = (0.5 + 1 / 16) if kind == "nvfp4" else 1.0
+    """Algorithmic bytes of one DiT GEMM: A codes (+ block scales), packed W
+    codes (+ scales), bf16 Y."""
+    per = {"nvfp4": 0.5 + 1 / 16, "fp8": 1.0, "mxfp4": 0.5 + 1 / 32, "mxfp8": 1.0 + 1 / 32}[kind]
     return m * k * per + n * k * per + 2 * m * n
 
 
@@ -103,13 +108,13 @@ def traffic_probe(kind):
     import synth
     torch.cuda.set_device(0)
     M = synth.DIT_TOKENS
-    fmt = q.QG_FMT_NVFP4 if kind == "nvfp4" else q.QG_FMT_FP8_E4M3
+    fmt = {"nvfp4": q.QG_FMT_NVFP4, "fp8": q.QG_FMT_FP8_E4M3, "mxfp4": q.QG_FMT_MXFP4, "mxfp8": q.QG_FMT_MXFP8}[kind]
     runs = []
     for li, (name, (n, k)) in enumerate(synth.DIT_LINEARS.items()):
         base = 16 * li
-        # NVFP4: the heavy-tailed activations of the step; FP8: N(0, 1)
+        # 4-bit formats: the heavy-tailed activations of the step; 8-bit: N(0, 1)
         x = synth.normal_bf16(M, k, synth.SIGMA_X, 0, base + synth.STREAM_X,
-                              outlier_frac=synth.HEAVY_TAIL_FRAC if kind == "nvfp4" else 0.0,
+                              outlier_frac=synth.HEAVY_TAIL_FRAC if kind in ("nvfp4", "mxfp4") else 0.0,
                               outlier_gain=synth.HEAVY_TAIL_GAIN, outlier_stream=base + synth.STREAM_OUTLIER)
         w = synth.normal_bf16(n, k, synth.SIGMA_W, 0, base + synth.STREAM_W)
         a = q.quantize(dev_bf16(x), fmt)
@@ -262,23 +267,24 @@ def mfma_summary(pmc_dir, out_md, kind):
     run over --traffic-probe."""
     import synth
     kern = KERNEL[kind]
-    flops_ctr = "MfmaFlopsF16" if kind == "nvfp4" else "SQ_INSTS_VALU_MFMA_MOPS_F8"
+    flops_ctr = FLOPS_CTR[kind]
     util, _ = read_counter(pmc_dir, "MfmaUtil", kern)
-    fl, _ = read_counter(pmc_dir, flops_ctr, kern)
     gui, _ = read_counter(pmc_dir, "GRBM_GUI_ACTIVE", kern)
-    if kind == "fp8":
+    fl, _ = read_counter(pmc_dir, flops_ctr, kern) if flops_ctr else ([float("nan")] * len(util), None)
+    if flops_ctr == "SQ_INSTS_VALU_MFMA_MOPS_F8":
         fl = [v * 512 for v in fl]
     assert len(util) == len(fl) == len(gui) == 12, (len(util), len(fl), len(gui))
     M = synth.DIT_TOKENS
     lines = ["# MFMA utilisation of `%s` at the transformer shapes (M = %d)" % (kern, M), "",
              "rocprofv3 counters over `bench.py --traffic-probe %s` (each of the four DiT-shaped %s GEMMs launched "
              "three times): `MfmaUtil` (SQ_VALU_MFMA_BUSY_CYCLES over the SIMDs / (GRBM_GUI_ACTIVE x SIMD count) x "
-             "100), executed MFMA flops (%s%s) and GRBM_GUI_ACTIVE (summed over the 8 XCDs)."
-             % (kind, kind.upper(), flops_ctr, " x 512" if kind == "fp8" else ""), "",
+             "100), executed MFMA flops (%s) and GRBM_GUI_ACTIVE (summed over the 8 XCDs)."
+             % (kind, kind.upper(), (flops_ctr + (" x 512" if flops_ctr == "SQ_INSTS_VALU_MFMA_MOPS_F8" else ""))
+                if flops_ctr else "no counter of this rocprofv3 counts the fp4-operand instructions: nan"), "",
              "Command (repo root, MI355X; $OUT any output directory):", "", "```",
-             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc MfmaUtil %s "
+             "cd /tmp && export TMPDIR=/tmp; cd $REPO && timeout -s KILL 120 rocprofv3 --pmc MfmaUtil %s"
              "GRBM_GUI_ACTIVE --output-format csv -d $OUT/pmc_mfma_%s -o run -- python3 bench.py "
-             "--traffic-probe %s" % (flops_ctr, kind, kind),
+             "--traffic-probe %s" % (flops_ctr + " " if flops_ctr else "", kind, kind),
              "python3 bench.py --mfma-summary $OUT/pmc_mfma_%s <this file> --kind %s" % (kind, kind), "```", "",
              "| linear (M x N x K) | launch | MfmaUtil % | MFMA flops / 2MNK | GUI-active cycles / 8 |",
              "|---|---:|---:|---:|---:|"]

@@ -139,25 +139,6 @@ __global__ void __launch_bounds__(256) k_finalize(const uint32_t* partial, int c
   }
 }
 
-// ---------------------------------------------------------------- element access
-// 16 consecutive bf16 of one row as fp32 (exact).
-template <bool VEC>
-__device__ inline void load16(const uint16_t* p, float (&v)[16]) {
-  if (VEC) {
-    const uint4 a = reinterpret_cast<const uint4*>(p)[0];
-    const uint4 b = reinterpret_cast<const uint4*>(p)[1];
-    const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      v[2 * i] = bf16_lo(w[i]);
-      v[2 * i + 1] = bf16_hi(w[i]);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = u2f((uint32_t)p[i] << 16);
-  }
-}
-
 // ---------------------------------------------------------------- units of 16
 // A unit: cnt (<= 16) consecutive bf16 of a row, held as 8 words (element
 // 2 i in the low half of word i, missing elements zero). VEC: the unit is

@@ -584,7 +584,9 @@ def main():
     # the launches of the dominant kernel (their durations give the roofline).
     # (ROCm's torch does not allow event-record nodes in captured graphs, so
     # the timed region is the eager launch loop; the graph-replayed step time
-    # is reported beside it in parts.)
+    # and the eager step without any event are reported beside it in parts.
+    # Graph segments between eager dominant launches were slower than either:
+    # each segment replay costs more than the queue gaps it removes.)
     step_events = []
     for _ in range(args.steps):
         ev = [None] * len(plan)
@@ -607,6 +609,15 @@ def main():
         for i in dom_idx:
             dom_live.setdefault(plan[i][0], []).append(evs[i][0].elapsed_time(evs[i][1]))
     timing_mode = "eager launches (events around the dominant kernel)"
+    # the same eager step without any event, for comparison
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(args.steps):
+        step([None] * len(plan))
+    e1.record()
+    torch.cuda.synchronize()
+    eager_step_ms = e0.elapsed_time(e1) / args.steps
     # the same step as a graph replay without any inner event (GPU time of the
     # launch list with no host launch latency between launches), for context
     graph_step_us = graph_us(lambda s: step([None] * len(plan), s), reps=args.steps)
@@ -654,6 +665,7 @@ def main():
                                        "latency included); graph_us: GPU time per call from graph replays")
     parts["launch_sum_ms_per_step"] = round(sum(sum(v) for v in durations.values()) / args.steps, 4)
     parts["graph_replay_ms_per_step"] = round(graph_step_us / 1e3, 4) if graph_step_us else None
+    parts["eager_no_event_ms_per_step"] = round(eager_step_ms, 4)
     parts["static_scales"] = static_scale_part(q, lib, st, dit, M, flops)
     parts["mx"] = mx_part(q, lib, st, dit, M, flops, parts["nvfp4"], parts["fp8"])
     parts["dit_block_chain"] = block_chain_part(q, dit, M)

@@ -20,6 +20,7 @@
 // Stream order separates the kernels; nothing waits on the host.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "quant_plan.hpp"
 
 namespace qg {
 
@@ -453,17 +454,7 @@ __global__ void __launch_bounds__(256) k_quant_dense(const uint16_t* __restrict_
 // of the n / 8 (the last region ends at n / 8), whose codes start at byte CB
 // times their first unit (CB = 8 for FP8, 4 for NVFP4). The host picks G so
 // that every region's codes hold the 4 P bytes of slots.
-__device__ inline int64_t slot_region_lo(int64_t pairs, int64_t j, int64_t g) { return 2 * (pairs * j / g); }
-constexpr int kSlotsAmaxLoads = 4;          // 16-byte loads per lane in flight
-constexpr int64_t kSlotsAmaxGroups = 1024;  // P, a multiple of 8
-constexpr int64_t kSlotsQuantGroups = 2048;
-// The P x G scattered 4-byte slot stores grow with the tensor: at 4608 x
-// 3072 (P = 1024 or 512, G = 1728 or 1024) the two launches took 17-22 us
-// against the chain's 12.4 (GPU time from graph replays); at 256 x 3072 5.7
-// against 6.7 us (FP8) and 6.4 against 7.7 (NVFP4), at 512 x 3072 6.2 against
-// 7.0 and 6.8 against 7.9, level from 3 Mi elements on (1024 x 4096: 8.2
-// against 7.8). Larger tensors take the chain.
-constexpr int64_t kSlotsMaxElements = int64_t(3) << 20;
+// (the plan: slot_region_lo, slots_plan and their limits in quant_plan.hpp)
 
 template <int U>
 __global__ void __launch_bounds__(256) k_amax_slots(const uint16_t* __restrict__ x, int64_t units,
@@ -816,13 +807,12 @@ hipError_t launch_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t col
     return hipGetLastError();
   }
   const int64_t n = rows * cols;
-  if (contig && aligned && n % 8 == 0 && n <= kSlotsMaxElements && reinterpret_cast<uintptr_t>(codes) % 8 == 0) {
+  if (contig && aligned && reinterpret_cast<uintptr_t>(codes) % 8 == 0) {
     // dense: two launches, the maxima handed over in every code region
-    const int64_t units = n / 8, pairs = units / 2;
+    const int64_t units = n / 8;
     const int cb = (fmt == 1) ? 8 : 4;
-    const int64_t P = std::min<int64_t>(kSlotsAmaxGroups, ((units + 256 * kSlotsAmaxLoads - 1) / (256 * kSlotsAmaxLoads) + 7) / 8 * 8);
-    const int64_t need = (4 * P + 2 * cb - 1) / (2 * cb);  // unit pairs per region that hold the slots
-    const int64_t G = std::min<int64_t>(std::min<int64_t>(kSlotsQuantGroups, (units + 1023) / 1024), pairs / need);
+    const SlotsPlan plan = slots_plan(n, cb);
+    const int64_t P = plan.P, G = plan.G;
     if (G >= 1) {
       hipLaunchKernelGGL(k_amax_slots<kSlotsAmaxLoads>, dim3((unsigned)P), dim3(256), 0, st, x, units, codes, cb, (int)G);
       if (fmt == 1)
